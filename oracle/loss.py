@@ -1,0 +1,85 @@
+"""Loss processes: which (worker, packet) transfers arrive.
+
+Test infrastructure (see the package docstring).
+
+Section 3 step (2) draws s_t^(i,j) ~ Bernoulli(1-p) for the gradient transfer
+from worker i to owner j, and step (4) draws r_t^(j,i) ~ Bernoulli(1-p) for
+the broadcast back; Algorithm 1 tests Uniform(0,1) < p to drop.  Here the
+indicator is drawn per (worker i, packet k) of the owner's shard, 1 meaning
+"arrived".  The uniform variate of Algorithm 1 is the top 32 bits of a
+Philox4x64-10 word divided by 2**32, so "Uniform < p" is the integer test
+hi32(w0) < ceil(p * 2**32); p = 0 never drops and p = 1 always drops.
+
+Counter of the draw for step t (0-based), worker i, packet k and direction
+dir (0 = gradient, 1 = broadcast):  ctr = (k, i, t, dir), key = (seed, 0).
+
+The bursty Gilbert-Elliott process goes beyond the paper's i.i.d. model (its
+Section 5 names bursty loss as open); each (dir, worker) runs a two-state
+Markov chain over the packet sequence (step-major, then packet), starting in
+Good before step 0.  Per packet the state first moves (Good->Bad when
+hi32(w0) < ceil(p_gb 2^32), Bad->Good when hi32(w0) < ceil(p_bg 2^32)), then
+the packet is lost when hi32(w1) < ceil(loss_state 2^32).
+"""
+from __future__ import annotations
+
+import math
+
+import numpy as np
+
+from .philox import philox4x64
+
+GRAD = 0
+BCAST = 1
+GOOD = 0
+BAD = 1
+
+
+def threshold(p: float) -> int:
+    """ceil(p * 2**32) for p in [0, 1]: hi32(w) < threshold  <=>  hi32(w)/2**32 < p."""
+    if not (0.0 <= p <= 1.0):
+        raise ValueError("probability outside [0, 1]")
+    return int(math.ceil(float(p) * 4294967296.0))
+
+
+def draw_words(seed: int, t: int, direction: int, workers, packets):
+    """Philox words (w0, w1) for every (worker, packet) pair: arrays [n][k]."""
+    i = np.asarray(workers, dtype=np.uint64)[:, None]
+    k = np.asarray(packets, dtype=np.uint64)[None, :]
+    w0, w1, _, _ = philox4x64(k, i, np.uint64(t), np.uint64(direction), seed, 0)
+    return w0, w1
+
+
+def hi32(w: np.ndarray) -> np.ndarray:
+    return (w >> np.uint64(32)).astype(np.int64)
+
+
+def bernoulli_arrivals(seed: int, t: int, direction: int, n: int, packets, p: float):
+    """uint8 [n][len(packets)], 1 = arrived, for i.i.d. loss probability p."""
+    w0, _ = draw_words(seed, t, direction, np.arange(n), packets)
+    lost = hi32(w0) < threshold(p)
+    return (~lost).astype(np.uint8)
+
+
+def ge_arrivals(seed: int, t: int, direction: int, n: int, num_packets: int,
+                p_gb: float, p_bg: float, loss_good: float, loss_bad: float,
+                state_in):
+    """Gilbert-Elliott arrivals for all packets of step t.
+
+    state_in: [n] states (0 Good, 1 Bad) at the end of step t-1 (all Good
+    before step 0).  Returns (uint8 [n][num_packets], state_out [n]).
+    The chain is walked packet by packet, all workers at once.
+    """
+    w0, w1 = draw_words(seed, t, direction, np.arange(n), np.arange(num_packets))
+    u_move = hi32(w0)
+    u_loss = hi32(w1)
+    t_gb, t_bg = threshold(p_gb), threshold(p_bg)
+    t_loss = np.array([threshold(loss_good), threshold(loss_bad)], dtype=np.int64)
+    state = np.array(state_in, dtype=np.int64).copy()
+    arrived = np.empty((n, num_packets), dtype=np.uint8)
+    for k in range(num_packets):
+        to_bad = (state == GOOD) & (u_move[:, k] < t_gb)
+        to_good = (state == BAD) & (u_move[:, k] < t_bg)
+        state = np.where(to_bad, BAD, np.where(to_good, GOOD, state))
+        lost = u_loss[:, k] < t_loss[state]
+        arrived[:, k] = np.where(lost, 0, 1)
+    return arrived, state.astype(np.uint8)
