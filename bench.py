@@ -1,0 +1,256 @@
+#!/usr/bin/env python3
+"""Benchmark of the lossy data-parallel step on one MI355X.
+
+One step = the whole hot path over one owner's shard: gradient and broadcast
+masks, per-packet unbiased aggregate, Adam update of the fp32 master, lossy
+broadcast into N bf16 replicas and drift statistics, i.e. one
+lossy_step_fused call (the fused kernel plus its small drift reduction).
+
+Default workload: N = 64 workers, one worker's ZeRO-2 shard of a
+6.74e9-element model (D = 105,250,000 bf16 gradients per worker), packets of
+4096 elements, i.i.d. loss p = 0.1 both ways, Adam, 64 bf16 replicas.
+
+Throughput is algorithmic HBM bytes per second: arrived gradient packets
+read, master + moments read and written, arrived replica packets written
+and, for drift, stale replica packets read (lost gradient packets are never
+needed, so never counted).  Prints one JSON line on stdout.
+"""
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import os
+import sys
+import time
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, HERE)
+
+HBM_PEAK_GBS = 8000.0
+METRIC = "aggregate+step+broadcast GB/s and % of HBM peak; N=64 7B-shard step"
+PMC_PROFILE = os.path.join(HERE, "profiles", "k_step_fused_n64_llama7b_shard_pmc.txt")
+KERNEL_SOURCES = ["paper_2507_07114_amd/csrc/kernels.hip",
+                  "paper_2507_07114_amd/csrc/lossy_device.h",
+                  "paper_2507_07114_amd/csrc/kernels.h"]
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def kernel_source_hash() -> str:
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(HERE, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def algorithmic_bytes(w, mg, mb, lens, drift: bool) -> dict:
+    """Bytes the step must move given realised masks (numpy [n][P] arrays)."""
+    import numpy as np
+    eb = w.elem_bytes
+    K = mg.sum(axis=0).astype(np.int64)
+    R = mb.sum(axis=0).astype(np.int64)
+    lens = lens.astype(np.int64)
+    nstate = {"sgd": 1, "momentum": 2, "adam": 3}[w.opt["kind"]]
+    d = int(lens.sum())
+    out = dict(
+        grads_read=int((K * lens).sum()) * eb,
+        state_rw=2 * 4 * nstate * d,
+        replicas_written=int((R * lens).sum()) * eb,
+        stale_read=int(((w.n - R) * lens).sum()) * eb if drift else 0,
+    )
+    out["total"] = sum(out.values())
+    return out
+
+
+def read_pmc_traffic(expect_hash: str):
+    """HBM bytes per dispatch from the committed rocprofv3 counter summary, or
+    None when it is absent or was taken on different kernel sources."""
+    if not os.path.exists(PMC_PROFILE):
+        return None
+    vals = {}
+    with open(PMC_PROFILE) as f:
+        for line in f:
+            if ":" in line and not line.startswith("#"):
+                k, v = line.split(":", 1)
+                vals[k.strip()] = v.strip()
+    if vals.get("kernel_source_sha256") != expect_hash:
+        return None
+    try:
+        return float(vals["hbm_bytes_per_dispatch"])
+    except (KeyError, ValueError):
+        return None
+
+
+def cpu_baseline(w, dev, packets_sample: int):
+    """The oracle, as it stands, on a bounded sample of packets of the same
+    workload (inputs copied from the device before any step runs)."""
+    import numpy as np
+    from oracle import drift as odrift
+    from oracle import loss as oloss
+    from oracle import step as ostep
+    P = w.num_packets
+    sample = list(range(0, P, max(1, P // packets_sample)))[:packets_sample]
+    idx = ostep.packet_elements(w.d, w.packet, sample)
+    import torch
+    ix = torch.as_tensor(idx, device=dev.theta.device)
+
+    def rows(t):
+        x = t.index_select(1, ix).cpu()
+        if w.gdtype == "bf16":
+            return (x.view(torch.int16).to(torch.int32) & 0xFFFF).numpy().astype(np.uint16)
+        return x.numpy()
+
+    g = rows(dev.grads)
+    reps = rows(dev.replicas)
+    th = dev.theta.index_select(0, ix).cpu().numpy()
+    m = None if dev.m is None else dev.m.index_select(0, ix).cpu().numpy()
+    v = None if dev.v is None else dev.v.index_select(0, ix).cpu().numpy()
+    p = w.loss["p"]
+    t0 = time.perf_counter()
+    c0 = time.process_time()
+    mg = oloss.bernoulli_arrivals(w.seed, 0, oloss.GRAD, w.n, sample, p)
+    mb = oloss.bernoulli_arrivals(w.seed, 0, oloss.BCAST, w.n, sample, p)
+    out = ostep.lossy_step(d=w.d, packet=w.packet, packets=sample, gdtype=w.gdtype, grads=g,
+                           theta=th, m=m, v=v, replicas=reps, arrived_g=mg, arrived_b=mb,
+                           opt=w.opt, t=0)
+    odrift.drift_stats(ostep.widen(out["replicas"], w.gdtype),
+                       ostep.widen(ostep.store(out["theta"], w.gdtype), w.gdtype), mb)
+    wall = time.perf_counter() - t0
+    cpu = time.process_time() - c0
+    lens = ostep.packet_lengths(w.d, w.packet, sample)
+    b = algorithmic_bytes(w, mg, mb, lens, True)["total"]
+    return dict(value=round(b / wall / 1e9, 4), unit="GB/s",
+                cores=max(1, int(round(cpu / wall))), kind="oracle",
+                sample=f"{len(sample)} of {P} packets (every {max(1, P // packets_sample)}th), "
+                       f"one step incl. masks and drift, {wall:.1f} s wall; "
+                       f"{len(os.sched_getaffinity(0))} host cores available")
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default=None)
+    ap.add_argument("--cpu-packets", type=int, default=768,
+                    help="packets of the workload the CPU oracle baseline runs on")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only: this build simulates the N workers of one "
+              f"owner's shard on a single device and has no multi-GPU path "
+              f"(asked for --gpus {args.gpus}).", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2507_07114_amd as ll
+    import workloads as wl
+    from workloads.device import DeviceState, loss_spec
+
+    if not torch.cuda.is_available():
+        log("no GPU visible")
+        sys.exit(1)
+    name = args.workload or wl.METRIC_WORKLOAD
+    w = wl.WORKLOADS[name]
+    if w.loss["kind"] != wl.BERNOULLI:
+        log("the benchmark times Bernoulli-loss workloads only")
+        sys.exit(1)
+    log(f"workload {name}: n={w.n} d={w.d} packet={w.packet} P={w.num_packets}")
+    dev = DeviceState(w)
+    torch.cuda.synchronize()
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        log(f"timing the CPU oracle on {args.cpu_packets} packets ...")
+        cpu = cpu_baseline(w, dev, args.cpu_packets)
+        log(f"cpu oracle: {cpu}")
+
+    # Realised masks of the timed steps, for the algorithmic byte count.
+    P = w.num_packets
+    spec = loss_spec(w)
+    lens = np.minimum((np.arange(P) + 1) * w.packet, w.d) - np.arange(P) * w.packet
+    mg_dev = torch.empty((w.n, P), dtype=torch.uint8, device="cuda")
+    mb_dev = torch.empty((w.n, P), dtype=torch.uint8, device="cuda")
+    per_step_bytes = []
+    for t in range(args.warmup, args.warmup + args.steps):
+        ll.ll_masks(w.n, P, t, ll.LL_DIR_GRAD, spec, mg_dev)
+        ll.ll_masks(w.n, P, t, ll.LL_DIR_BCAST, spec, mb_dev)
+        per_step_bytes.append(algorithmic_bytes(w, mg_dev.cpu().numpy(), mb_dev.cpu().numpy(),
+                                                lens, True))
+
+    for t in range(args.warmup):
+        dev.fused(t, masks_out=False)
+    torch.cuda.synchronize()
+
+    stream = torch.cuda.current_stream()
+    starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    ends = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    for j in range(args.steps):
+        starts[j].record(stream)
+        dev.fused(args.warmup + j, masks_out=False)
+        ends[j].record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    ms = [s.elapsed_time(e) for s, e in zip(starts, ends)]
+    drift = ll.read_drift(dev.drift)
+
+    total_bytes = sum(b["total"] for b in per_step_bytes)
+    ms_per_step = wall * 1e3 / args.steps
+    value = total_bytes / wall / 1e9
+    mean_bytes = total_bytes / args.steps
+    launch_ms = float(np.mean(ms))
+    achieved = mean_bytes / (launch_ms * 1e-3) / 1e9
+    khash = kernel_source_hash()
+    traffic = read_pmc_traffic(khash)
+    mean_b = {k: int(np.mean([b[k] for b in per_step_bytes])) for k in per_step_bytes[0]}
+    log(f"per-launch event times (ms): min {min(ms):.3f} median {float(np.median(ms)):.3f} "
+        f"max {max(ms):.3f}; algorithmic bytes/step {mean_b}")
+    log(f"drift after last step: {drift}")
+    result = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {"workload": name, "n": w.n, "d": w.d, "packet": w.packet,
+                   "packets": P, "loss": w.loss, "optimizer": w.opt["kind"],
+                   "grad_dtype": w.gdtype, "replica_dtype": w.gdtype,
+                   "drift": True, "parallelism": "single-gpu simulation of n workers"},
+        "pct_hbm_peak": round(100.0 * value / HBM_PEAK_GBS, 2),
+        "elements_per_s": round(w.n * w.d / (ms_per_step * 1e-3), 1),
+        "shard_elements_per_s": round(w.d / (ms_per_step * 1e-3), 1),
+        "algorithmic_bytes_per_step": mean_b,
+        "roofline": {
+            "bound": "hbm",
+            "kernel": "k_step_fused (+ k_drift_final)",
+            "achieved": round(achieved, 2),
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4),
+            "traffic": None if traffic is None else round(traffic),
+            "launch_ms": round(launch_ms, 4),
+            "kernel_source_sha256": khash,
+        },
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

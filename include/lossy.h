@@ -1,0 +1,226 @@
+/*
+ * lossy.h -- C ABI of the packet-loss-tolerant data-parallel step on one
+ * MI355X (gfx950).
+ *
+ * The operations follow "Distributed Training under Packet Loss"
+ * (Weintraub, Banner, Orda, 2025), Section 3, for the shard owned by one
+ * worker W_j.  N workers each hold a gradient row for that shard; the shard
+ * of D elements is cut into packets of L elements (P = ceil(D / L) packets,
+ * the last may be short).  Per step:
+ *
+ *   (a) gradient packets from each worker arrive or are lost (step (2));
+ *   (b) the owner forms the unbiased aggregate: per packet, the sum of the
+ *       rows that arrived divided by how many arrived (step (2) and
+ *       "Unbiased Gradient Aggregation");
+ *   (c) the owner updates its fp32 master shard (step (3));
+ *   (d) the owner broadcasts the new shard; each of the N replica buffers
+ *       takes a packet only where that broadcast arrived, otherwise keeps
+ *       its stale value (step (4));
+ *   (e) drift statistics over the N replicas (Theorem 3.1).
+ *
+ * Conventions for every entry point:
+ *   - All pointers are DEVICE pointers unless marked "host".  The caller owns
+ *     all memory; the library allocates none.  Scratch memory comes from a
+ *     caller-supplied workspace of ll_workspace_bytes() bytes.
+ *   - `stream` is a hipStream_t (NULL = the default stream).  Every call only
+ *     enqueues work on it and returns without synchronising; device outputs
+ *     are valid once the stream has reached that point.
+ *   - Row-major [N][ld] buffers: row i starts at element i * ld.  ld >= D.
+ *   - Masks are uint8 [N][P] (row i = worker/replica i, column k = packet),
+ *     1 = arrived, 0 = lost.
+ *   - Return codes: LL_OK (0); LL_EINVAL (-1) for a bad size or argument
+ *     (N outside [1, 1024], D < 0, L < 8 or L not a multiple of 8, ld < D,
+ *     a probability outside [0, 1], an unknown kind or dtype, a required
+ *     pointer that is NULL, a workspace that is too small, or a launch that
+ *     would exceed the grid limit); LL_EALIGN (-2) when a buffer address is
+ *     not 16-byte aligned or ld is not a multiple of 8 elements; LL_EHIP
+ *     (-3) when the HIP runtime reports an error.  ll_last_error() then
+ *     returns a message (thread-local, valid until the next call on that
+ *     thread).  No exception crosses this boundary.
+ *   - D = 0 is a valid no-op (drift outputs are then written as zeros).
+ *   - Calls that share output buffers must be ordered by the caller (same
+ *     stream or events); the library keeps no state between calls.
+ */
+#ifndef LOSSY_H
+#define LOSSY_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#if defined(__GNUC__)
+#define LL_API __attribute__((visibility("default")))
+#else
+#define LL_API
+#endif
+
+enum { LL_OK = 0, LL_EINVAL = -1, LL_EALIGN = -2, LL_EHIP = -3 };
+enum { LL_F32 = 0, LL_BF16 = 1 };
+enum { LL_LOSS_BERNOULLI = 0, LL_LOSS_GILBERT_ELLIOTT = 1 };
+enum { LL_SGD = 0, LL_SGD_MOMENTUM = 1, LL_ADAM = 2 };
+enum { LL_DIR_GRAD = 0, LL_DIR_BCAST = 1 };
+
+/*
+ * Loss process (Section 3 steps (2) and (4): each transfer succeeds with
+ * probability 1 - p; Algorithm 1 drops when Uniform(0,1) < p).
+ *
+ * The draw for step t (0-based), worker i, packet k and direction dir is the
+ * Philox4x64-10 block (Salmon et al., SC'11) at counter (k, i, t, dir) under
+ * key (seed, 0).  With u0, u1 the top 32 bits of its words 0 and 1:
+ *   BERNOULLI        lost  <=>  u0 < ceil(p * 2^32)   (so u0 / 2^32 < p).
+ *   GILBERT_ELLIOTT  per (dir, worker) a two-state chain over packets in
+ *                    step-major order, Good before step 0; per packet the
+ *                    state first moves (Good->Bad iff u0 < ceil(p_gb 2^32),
+ *                    Bad->Good iff u0 < ceil(p_bg 2^32)), then the packet is
+ *                    lost iff u1 < ceil(loss_state 2^32).  Bursty loss goes
+ *                    beyond the paper's i.i.d. model (its Section 5).
+ * Fields not used by `kind` are ignored.
+ */
+typedef struct {
+    int32_t kind;
+    double p;
+    double p_gb, p_bg, loss_good, loss_bad;
+    uint64_t seed;
+} ll_loss;
+
+/*
+ * Owner update (Section 3 step (3): theta <- theta - eta * g_hat).
+ *   LL_SGD           theta -= lr * g
+ *   LL_SGD_MOMENTUM  b = momentum * b + g;  theta -= lr * b   (b starts at 0)
+ *   LL_ADAM          m = beta1 m + (1-beta1) g;  v = beta2 v + (1-beta2) g^2;
+ *                    theta -= lr * (m / (1-beta1^(t+1))) /
+ *                             (sqrt(v / (1-beta2^(t+1))) + eps)
+ * fallback_lambda: when no contribution of a packet arrived, the paper says
+ * to fall back to a small regulariser ("Unbiased Gradient Aggregation");
+ * the aggregate is then fallback_lambda * theta (0 gives g_hat = 0).
+ */
+typedef struct {
+    int32_t kind;
+    float lr, momentum, beta1, beta2, eps;
+    float fallback_lambda;
+} ll_opt;
+
+/*
+ * Drift statistics over the N replicas x_i of every element e (the
+ * discrepancy D = theta^(i,j) - theta^(k,j) of Theorem 3.1):
+ *   max_abs            max_e (max_i x_ie - min_i x_ie)
+ *   mean_sq            sum_e sum_{i<k} (x_ie - x_ke)^2 / (D * N(N-1)/2)
+ *                      (0 when N = 1 or D = 0)
+ *   rms                sqrt(mean_sq)
+ *   mean_abs_to_master sum_{i,e} |x_ie - c(theta_e)| / (N D), c = rounding to
+ *                      the replica dtype; NaN when no master is given
+ *   stale_packets      number of (replica, packet) broadcasts lost
+ *   empty_packets      packets whose gradient contributions were all lost
+ *                      (filled by lossy_step_fused; drift_stats writes 0)
+ * Sums are taken in fp64 in a fixed order, so results are deterministic.
+ */
+typedef struct {
+    double max_abs, mean_sq, rms, mean_abs_to_master;
+    uint64_t stale_packets, empty_packets;
+} ll_drift;
+
+/*
+ * Arrival masks for one step and direction (Section 3 step (2) for
+ * dir = LL_DIR_GRAD, step (4) for LL_DIR_BCAST) under `loss` (host).
+ *   n, num_packets   mask shape [n][num_packets]; arrived (device, out).
+ *   step             0-based step index t.
+ *   ge_state         Gilbert-Elliott only: uint8 [n] (device, in/out), the
+ *                    chain state (0 Good, 1 Bad) at the end of the previous
+ *                    step; updated to the end of this step.  Ignored (may be
+ *                    NULL) for Bernoulli.
+ */
+LL_API int ll_masks(int32_t n, int64_t num_packets, uint64_t step, int32_t dir,
+             const ll_loss* loss, uint8_t* ge_state, uint8_t* arrived,
+             void* stream);
+
+/*
+ * Unbiased aggregate (Section 3 step (2); "Unbiased Gradient Aggregation"):
+ *   g_hat[e] = (sum_{i : arrived[i][k(e)]} grads[i][e]) / K[k(e)],
+ *   K[k] = sum_i arrived[i][k]; when K = 0, g_hat[e] = fallback_lambda * theta[e].
+ * The sum runs over arrived rows in ascending i, in fp32.
+ *   grads    [n][ld_g] of gdtype (LL_F32 or LL_BF16).
+ *   arrived  uint8 [n][P].
+ *   theta    fp32 [d]; read only when fallback_lambda != 0 (else may be NULL).
+ *   g_hat    fp32 [d] (out).  counts: int32 [P] (out, may be NULL).
+ * Lost rows are never read.
+ */
+LL_API int lossy_aggregate(int32_t n, int64_t d, int64_t packet, int32_t gdtype,
+                    const void* grads, int64_t ld_g, const uint8_t* arrived,
+                    float fallback_lambda, const float* theta, float* g_hat,
+                    int32_t* counts, void* stream);
+
+/*
+ * Owner update of the fp32 master shard (Section 3 step (3)), in place.
+ *   opt (host); step = 0-based t (Adam's bias correction uses t + 1).
+ *   m  momentum buffer (LL_SGD_MOMENTUM) or Adam first moment; NULL for SGD.
+ *   v  Adam second moment; NULL otherwise.   g_hat fp32 [d].
+ */
+LL_API int shard_step(const ll_opt* opt, int64_t d, uint64_t step, float* theta,
+               float* m, float* v, const float* g_hat, void* stream);
+
+/*
+ * Lossy parameter broadcast (Section 3 step (4)): for every replica i and
+ * packet k with arrived_bc[i][k] = 1, replicas[i][packet k] <- c(theta)
+ * (c = identity for LL_F32, round-to-nearest-even for LL_BF16); packets whose
+ * broadcast was lost are neither read nor written (they keep stale values).
+ *   theta fp32 [d]; replicas [n][ld_r] of rdtype; arrived_bc uint8 [n][P].
+ */
+LL_API int lossy_broadcast(int32_t n, int64_t d, int64_t packet, const float* theta,
+                    int32_t rdtype, void* replicas, int64_t ld_r,
+                    const uint8_t* arrived_bc, void* stream);
+
+/*
+ * Drift statistics (see ll_drift) over all n replicas [n][ld_r] of rdtype.
+ *   theta       fp32 [d] master used as the reference c(theta); may be NULL
+ *               (then replica 0 is the reference and mean_abs_to_master is NaN).
+ *   arrived_bc  uint8 [n][P], only used to count stale packets; may be NULL.
+ *   workspace   device scratch of ws_bytes >= ll_workspace_bytes(n, d, packet).
+ *   out         ll_drift (device, out).
+ */
+LL_API int drift_stats(int32_t n, int64_t d, int64_t packet, int32_t rdtype,
+                const void* replicas, int64_t ld_r, const float* theta,
+                const uint8_t* arrived_bc, void* workspace, size_t ws_bytes,
+                ll_drift* out, void* stream);
+
+/*
+ * The whole step in one pass over HBM: masks (both directions), aggregate,
+ * update, broadcast and, if `drift` is non-NULL, drift statistics of the
+ * replicas after the broadcast.  Equivalent to
+ *   ll_masks(GRAD) -> lossy_aggregate -> shard_step -> ll_masks(BCAST)
+ *   -> lossy_broadcast -> drift_stats
+ * with the same arithmetic, so its outputs are bit-identical to that chain.
+ *   loss_g, loss_b, opt     host structs.
+ *   ge_state_g, ge_state_b  uint8 [n] each (device, in/out) for
+ *                           Gilbert-Elliott processes, else may be NULL.
+ *   arrived_g, arrived_b    uint8 [n][P] (out, may be NULL): the masks drawn.
+ *   counts                  int32 [P] (out, may be NULL): gradient arrivals.
+ *   workspace, ws_bytes     scratch, ws_bytes >= ll_workspace_bytes(n, d, packet).
+ *   drift                   ll_drift (device, out) or NULL to skip drift.
+ * Lost gradient packets are never read; lost broadcast packets are read only
+ * for drift and never written.
+ */
+LL_API int lossy_step_fused(int32_t n, int64_t d, int64_t packet, uint64_t step,
+                     const ll_loss* loss_g, const ll_loss* loss_b,
+                     uint8_t* ge_state_g, uint8_t* ge_state_b,
+                     int32_t gdtype, const void* grads, int64_t ld_g,
+                     const ll_opt* opt, float* theta, float* m, float* v,
+                     int32_t rdtype, void* replicas, int64_t ld_r,
+                     uint8_t* arrived_g, uint8_t* arrived_b, int32_t* counts,
+                     void* workspace, size_t ws_bytes, ll_drift* drift,
+                     void* stream);
+
+/* Bytes of device workspace that drift_stats and lossy_step_fused need for
+ * these sizes (0 on invalid sizes). */
+LL_API size_t ll_workspace_bytes(int32_t n, int64_t d, int64_t packet);
+
+/* Message describing the last error on this thread ("" if none). */
+LL_API const char* ll_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* LOSSY_H */

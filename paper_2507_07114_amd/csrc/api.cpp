@@ -1,0 +1,367 @@
+// C ABI of the lossy step (declared in include/lossy.h): argument checks,
+// launch geometry and error reporting around the HIP kernels.
+#include "lossy.h"
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <string>
+
+#include "kernels.h"
+
+using namespace lossy;
+
+static_assert(sizeof(ll_drift) == sizeof(DriftOut), "ll_drift layout");
+static_assert(sizeof(DriftPartial) == 32, "partial layout");
+
+namespace {
+
+thread_local std::string g_error;
+
+int fail(int code, const char* fmt, ...) {
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof(buf), fmt, ap);
+    va_end(ap);
+    g_error = buf;
+    return code;
+}
+
+int ok() {
+    g_error.clear();
+    return LL_OK;
+}
+
+int hip_check(hipError_t e, const char* what) {
+    if (e != hipSuccess) return fail(LL_EHIP, "%s: %s", what, hipGetErrorString(e));
+    return ok();
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// ceil(p * 2^32): hi32(w) < thr  <=>  hi32(w) / 2^32 < p.
+uint64_t threshold(double p) { return (uint64_t)std::ceil(p * 4294967296.0); }
+
+bool prob_ok(double p) { return p >= 0.0 && p <= 1.0; }
+
+struct Geometry {
+    int64_t P = 0;    // packets
+    int cpp = 0;      // workgroup chunks per packet
+    int64_t blocks = 0;
+};
+
+// Shared checks of (n, d, packet); fills the launch geometry.
+int check_shape(int32_t n, int64_t d, int64_t packet, Geometry* g) {
+    if (n < 1 || n > kMaxWorkers) return fail(LL_EINVAL, "n=%d outside [1, %d]", n, kMaxWorkers);
+    if (d < 0) return fail(LL_EINVAL, "d=%lld is negative", (long long)d);
+    if (packet < 8 || packet % 8 != 0)
+        return fail(LL_EINVAL, "packet=%lld must be a positive multiple of 8", (long long)packet);
+    g->P = (d + packet - 1) / packet;
+    g->cpp = (int)((packet + kChunk - 1) / kChunk);
+    g->blocks = g->P * g->cpp;
+    if (g->blocks > 0x7FFFFFFFll)
+        return fail(LL_EINVAL, "too many workgroups (%lld)", (long long)g->blocks);
+    return LL_OK;
+}
+
+int check_rows(const char* name, const void* p, int64_t ld, int64_t d) {
+    if (!p) return fail(LL_EINVAL, "%s is NULL", name);
+    if (ld < d) return fail(LL_EINVAL, "%s: ld=%lld < d=%lld", name, (long long)ld, (long long)d);
+    if (ld % 8 != 0) return fail(LL_EALIGN, "%s: ld=%lld not a multiple of 8", name, (long long)ld);
+    if (!aligned16(p)) return fail(LL_EALIGN, "%s is not 16-byte aligned", name);
+    return LL_OK;
+}
+
+int check_vec(const char* name, const void* p, bool required) {
+    if (!p) return required ? fail(LL_EINVAL, "%s is NULL", name) : LL_OK;
+    if (!aligned16(p)) return fail(LL_EALIGN, "%s is not 16-byte aligned", name);
+    return LL_OK;
+}
+
+int check_dtype(const char* name, int32_t t) {
+    if (t != LL_F32 && t != LL_BF16) return fail(LL_EINVAL, "%s: unknown dtype %d", name, t);
+    return LL_OK;
+}
+
+int check_loss(const char* name, const ll_loss* l) {
+    if (!l) return fail(LL_EINVAL, "%s is NULL", name);
+    if (l->kind == LL_LOSS_BERNOULLI) {
+        if (!prob_ok(l->p)) return fail(LL_EINVAL, "%s: p outside [0, 1]", name);
+    } else if (l->kind == LL_LOSS_GILBERT_ELLIOTT) {
+        if (!prob_ok(l->p_gb) || !prob_ok(l->p_bg) || !prob_ok(l->loss_good) ||
+            !prob_ok(l->loss_bad))
+            return fail(LL_EINVAL, "%s: Gilbert-Elliott probability outside [0, 1]", name);
+    } else {
+        return fail(LL_EINVAL, "%s: unknown loss kind %d", name, l->kind);
+    }
+    return LL_OK;
+}
+
+int make_opt(const ll_opt* opt, uint64_t step, const float* m, const float* v, OptParams* o) {
+    if (!opt) return fail(LL_EINVAL, "opt is NULL");
+    if (opt->kind != LL_SGD && opt->kind != LL_SGD_MOMENTUM && opt->kind != LL_ADAM)
+        return fail(LL_EINVAL, "unknown optimizer kind %d", opt->kind);
+    if (opt->kind >= LL_SGD_MOMENTUM) {
+        int r = check_vec("m", m, true);
+        if (r) return r;
+    }
+    if (opt->kind == LL_ADAM) {
+        int r = check_vec("v", v, true);
+        if (r) return r;
+    }
+    o->kind = opt->kind;
+    o->lr = opt->lr;
+    o->momentum = opt->momentum;
+    o->beta1 = opt->beta1;
+    o->beta2 = opt->beta2;
+    o->eps = opt->eps;
+    const double t1 = (double)step + 1.0;
+    o->bc1 = (float)(1.0 - std::pow((double)opt->beta1, t1));
+    o->bc2 = (float)(1.0 - std::pow((double)opt->beta2, t1));
+    if (opt->kind == LL_ADAM && (!(o->bc1 > 0.0f) || !(o->bc2 > 0.0f)))
+        return fail(LL_EINVAL, "Adam betas must lie in [0, 1)");
+    return LL_OK;
+}
+
+GeParams make_ge(const ll_loss* l) {
+    GeParams g;
+    g.seed = l->seed;
+    g.thr_gb = threshold(l->p_gb);
+    g.thr_bg = threshold(l->p_bg);
+    g.thr_loss_good = threshold(l->loss_good);
+    g.thr_loss_bad = threshold(l->loss_bad);
+    return g;
+}
+
+size_t round256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+// Workspace layout: [drift partials][gradient masks][broadcast masks].
+struct WsLayout {
+    size_t partials = 0, masks = 0, total = 0;
+};
+
+WsLayout ws_layout(int32_t n, const Geometry& g) {
+    WsLayout w;
+    w.partials = round256((size_t)g.blocks * sizeof(DriftPartial));
+    w.masks = round256((size_t)n * (size_t)g.P);
+    w.total = w.partials + 2 * w.masks;
+    return w;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* ll_last_error(void) { return g_error.c_str(); }
+
+size_t ll_workspace_bytes(int32_t n, int64_t d, int64_t packet) {
+    Geometry g;
+    if (check_shape(n, d, packet, &g) != LL_OK) return 0;
+    return ws_layout(n, g).total;
+}
+
+int ll_masks(int32_t n, int64_t num_packets, uint64_t step, int32_t dir, const ll_loss* loss,
+             uint8_t* ge_state, uint8_t* arrived, void* stream) {
+    if (n < 1 || n > kMaxWorkers) return fail(LL_EINVAL, "n=%d outside [1, %d]", n, kMaxWorkers);
+    if (num_packets < 0) return fail(LL_EINVAL, "num_packets is negative");
+    if (dir != LL_DIR_GRAD && dir != LL_DIR_BCAST) return fail(LL_EINVAL, "unknown direction %d", dir);
+    int r = check_loss("loss", loss);
+    if (r) return r;
+    if (!arrived) return fail(LL_EINVAL, "arrived is NULL");
+    if (loss->kind == LL_LOSS_GILBERT_ELLIOTT && !ge_state)
+        return fail(LL_EINVAL, "ge_state is NULL for a Gilbert-Elliott process");
+    if (num_packets == 0) return ok();
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    if (loss->kind == LL_LOSS_BERNOULLI)
+        return hip_check(launch_masks_bernoulli(n, num_packets, step, dir, loss->seed,
+                                                threshold(loss->p), arrived, s),
+                         "ll_masks");
+    return hip_check(launch_masks_ge(n, num_packets, step, dir, make_ge(loss), ge_state, arrived, s),
+                     "ll_masks");
+}
+
+int lossy_aggregate(int32_t n, int64_t d, int64_t packet, int32_t gdtype, const void* grads,
+                    int64_t ld_g, const uint8_t* arrived, float fallback_lambda,
+                    const float* theta, float* g_hat, int32_t* counts, void* stream) {
+    Geometry g;
+    int r = check_shape(n, d, packet, &g);
+    if (r) return r;
+    if ((r = check_dtype("gdtype", gdtype))) return r;
+    if (d == 0) return ok();
+    if ((r = check_rows("grads", grads, ld_g, d))) return r;
+    if (!arrived) return fail(LL_EINVAL, "arrived is NULL");
+    if ((r = check_vec("g_hat", g_hat, true))) return r;
+    if ((r = check_vec("theta", theta, fallback_lambda != 0.0f))) return r;
+    AggParams p;
+    p.n = n;
+    p.d = d;
+    p.L = packet;
+    p.P = g.P;
+    p.cpp = g.cpp;
+    p.grads = grads;
+    p.ld = ld_g;
+    p.arrived = arrived;
+    p.lam = fallback_lambda;
+    p.theta = theta;
+    p.g_hat = g_hat;
+    p.counts = counts;
+    return hip_check(launch_aggregate(gdtype, p, g.blocks, reinterpret_cast<hipStream_t>(stream)),
+                     "lossy_aggregate");
+}
+
+int shard_step(const ll_opt* opt, int64_t d, uint64_t step, float* theta, float* m, float* v,
+               const float* g_hat, void* stream) {
+    if (d < 0) return fail(LL_EINVAL, "d is negative");
+    if (d == 0) return ok();
+    OptParams o;
+    int r = make_opt(opt, step, m, v, &o);
+    if (r) return r;
+    if ((r = check_vec("theta", theta, true))) return r;
+    if ((r = check_vec("g_hat", g_hat, true))) return r;
+    if ((d + kChunk - 1) / kChunk > 0x7FFFFFFFll) return fail(LL_EINVAL, "d too large");
+    return hip_check(launch_shard_step(d, o, theta, m, v, g_hat,
+                                       reinterpret_cast<hipStream_t>(stream)),
+                     "shard_step");
+}
+
+int lossy_broadcast(int32_t n, int64_t d, int64_t packet, const float* theta, int32_t rdtype,
+                    void* replicas, int64_t ld_r, const uint8_t* arrived_bc, void* stream) {
+    Geometry g;
+    int r = check_shape(n, d, packet, &g);
+    if (r) return r;
+    if ((r = check_dtype("rdtype", rdtype))) return r;
+    if (d == 0) return ok();
+    if ((r = check_vec("theta", theta, true))) return r;
+    if ((r = check_rows("replicas", replicas, ld_r, d))) return r;
+    if (!arrived_bc) return fail(LL_EINVAL, "arrived_bc is NULL");
+    BcastParams p;
+    p.n = n;
+    p.d = d;
+    p.L = packet;
+    p.P = g.P;
+    p.cpp = g.cpp;
+    p.theta = theta;
+    p.replicas = replicas;
+    p.ld = ld_r;
+    p.arrived = arrived_bc;
+    return hip_check(launch_broadcast(rdtype, p, g.blocks, reinterpret_cast<hipStream_t>(stream)),
+                     "lossy_broadcast");
+}
+
+int drift_stats(int32_t n, int64_t d, int64_t packet, int32_t rdtype, const void* replicas,
+                int64_t ld_r, const float* theta, const uint8_t* arrived_bc, void* workspace,
+                size_t ws_bytes, ll_drift* out, void* stream) {
+    Geometry g;
+    int r = check_shape(n, d, packet, &g);
+    if (r) return r;
+    if ((r = check_dtype("rdtype", rdtype))) return r;
+    if (!out) return fail(LL_EINVAL, "out is NULL");
+    if ((r = check_vec("out", out, true))) return r;
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    if (d == 0) return hip_check(launch_drift_zero(reinterpret_cast<DriftOut*>(out), s), "drift_stats");
+    if ((r = check_rows("replicas", replicas, ld_r, d))) return r;
+    if ((r = check_vec("theta", theta, false))) return r;
+    const WsLayout w = ws_layout(n, g);
+    if (!workspace || ws_bytes < w.total)
+        return fail(LL_EINVAL, "workspace of %zu bytes is smaller than %zu", ws_bytes, w.total);
+    if ((r = check_vec("workspace", workspace, true))) return r;
+    DriftParams p;
+    p.n = n;
+    p.d = d;
+    p.L = packet;
+    p.P = g.P;
+    p.cpp = g.cpp;
+    p.replicas = replicas;
+    p.ld = ld_r;
+    p.theta = theta;
+    p.arrived = arrived_bc;
+    p.partials = reinterpret_cast<DriftPartial*>(workspace);
+    return hip_check(launch_drift(rdtype, p, g.blocks, n, d, theta != nullptr,
+                                  reinterpret_cast<DriftOut*>(out), s),
+                     "drift_stats");
+}
+
+int lossy_step_fused(int32_t n, int64_t d, int64_t packet, uint64_t step, const ll_loss* loss_g,
+                     const ll_loss* loss_b, uint8_t* ge_state_g, uint8_t* ge_state_b,
+                     int32_t gdtype, const void* grads, int64_t ld_g, const ll_opt* opt,
+                     float* theta, float* m, float* v, int32_t rdtype, void* replicas,
+                     int64_t ld_r, uint8_t* arrived_g, uint8_t* arrived_b, int32_t* counts,
+                     void* workspace, size_t ws_bytes, ll_drift* drift, void* stream) {
+    Geometry g;
+    int r = check_shape(n, d, packet, &g);
+    if (r) return r;
+    if ((r = check_loss("loss_g", loss_g))) return r;
+    if ((r = check_loss("loss_b", loss_b))) return r;
+    if ((r = check_dtype("gdtype", gdtype))) return r;
+    if ((r = check_dtype("rdtype", rdtype))) return r;
+    const bool ge_g = loss_g->kind == LL_LOSS_GILBERT_ELLIOTT;
+    const bool ge_b = loss_b->kind == LL_LOSS_GILBERT_ELLIOTT;
+    if (ge_g && !ge_state_g) return fail(LL_EINVAL, "ge_state_g is NULL for a Gilbert-Elliott process");
+    if (ge_b && !ge_state_b) return fail(LL_EINVAL, "ge_state_b is NULL for a Gilbert-Elliott process");
+    if (drift && (r = check_vec("drift", drift, true))) return r;
+    hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    if (d == 0) {
+        if (drift) return hip_check(launch_drift_zero(reinterpret_cast<DriftOut*>(drift), s), "lossy_step_fused");
+        return ok();
+    }
+    if ((r = check_rows("grads", grads, ld_g, d))) return r;
+    if ((r = check_rows("replicas", replicas, ld_r, d))) return r;
+    if ((r = check_vec("theta", theta, true))) return r;
+    OptParams o;
+    if ((r = make_opt(opt, step, m, v, &o))) return r;
+    const WsLayout w = ws_layout(n, g);
+    const bool need_ws = drift || (ge_g && !arrived_g) || (ge_b && !arrived_b);
+    if (need_ws) {
+        if (!workspace || ws_bytes < w.total)
+            return fail(LL_EINVAL, "workspace of %zu bytes is smaller than %zu", ws_bytes, w.total);
+        if ((r = check_vec("workspace", workspace, true))) return r;
+    }
+    uint8_t* ws = reinterpret_cast<uint8_t*>(workspace);
+
+    FusedParams p;
+    p.n = n;
+    p.d = d;
+    p.L = packet;
+    p.P = g.P;
+    p.cpp = g.cpp;
+    p.step = step;
+    p.out_g = arrived_g;
+    p.out_b = arrived_b;
+    p.counts = counts;
+    p.grads = grads;
+    p.ld_g = ld_g;
+    p.opt = o;
+    p.lam = opt->fallback_lambda;
+    p.theta = theta;
+    p.m = m;
+    p.v = v;
+    p.replicas = replicas;
+    p.ld_r = ld_r;
+    p.partials = drift ? reinterpret_cast<DriftPartial*>(ws) : nullptr;
+
+    const ll_loss* losses[2] = {loss_g, loss_b};
+    uint8_t* states[2] = {ge_state_g, ge_state_b};
+    uint8_t* outs[2] = {arrived_g, arrived_b};
+    for (int dir = 0; dir < 2; ++dir) {
+        const ll_loss* l = losses[dir];
+        if (l->kind == LL_LOSS_BERNOULLI) {
+            p.src[dir] = MaskSource{true, l->seed, threshold(l->p), nullptr};
+        } else {
+            // Sequential chain: a scan kernel writes the masks, the step reads them.
+            uint8_t* dst = outs[dir] ? outs[dir] : ws + w.partials + dir * w.masks;
+            r = hip_check(launch_masks_ge(n, g.P, step, dir, make_ge(l), states[dir], dst, s),
+                          "lossy_step_fused (Gilbert-Elliott masks)");
+            if (r) return r;
+            p.src[dir] = MaskSource{false, 0, 0, dst};
+            if (dir == 0) p.out_g = nullptr;  // already written by the scan
+            else p.out_b = nullptr;
+        }
+    }
+    return hip_check(launch_fused(gdtype, rdtype, p, g.blocks, reinterpret_cast<DriftOut*>(drift), s),
+                     "lossy_step_fused");
+}
+
+}  // extern "C"

@@ -1,0 +1,91 @@
+// Internal interface between the C ABI (api.cpp) and the HIP kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "lossy_device.h"
+
+namespace lossy {
+
+// Mirror of ll_drift (device-written).
+struct DriftOut {
+    double max_abs, mean_sq, rms, mean_abs_to_master;
+    unsigned long long stale_packets, empty_packets;
+};
+
+struct GeParams {
+    uint64_t seed;
+    uint64_t thr_gb, thr_bg, thr_loss_good, thr_loss_bad;
+};
+
+struct AggParams {
+    int n;
+    int64_t d, L, P;
+    int cpp;  // chunks per packet
+    const void* grads;
+    int64_t ld;
+    const uint8_t* arrived;
+    float lam;
+    const float* theta;
+    float* g_hat;
+    int32_t* counts;
+};
+
+struct BcastParams {
+    int n;
+    int64_t d, L, P;
+    int cpp;
+    const float* theta;
+    void* replicas;
+    int64_t ld;
+    const uint8_t* arrived;
+};
+
+struct DriftParams {
+    int n;
+    int64_t d, L, P;
+    int cpp;
+    const void* replicas;
+    int64_t ld;
+    const float* theta;
+    const uint8_t* arrived;
+    DriftPartial* partials;
+};
+
+struct FusedParams {
+    int n;
+    int64_t d, L, P;
+    int cpp;
+    uint64_t step;
+    MaskSource src[2];  // [0] gradient, [1] broadcast
+    uint8_t* out_g;
+    uint8_t* out_b;
+    int32_t* counts;
+    const void* grads;
+    int64_t ld_g;
+    OptParams opt;
+    float lam;
+    float* theta;
+    float* m;
+    float* v;
+    void* replicas;
+    int64_t ld_r;
+    DriftPartial* partials;
+};
+
+hipError_t launch_masks_bernoulli(int n, int64_t num_packets, uint64_t step, int dir,
+                                  uint64_t seed, uint64_t thr, uint8_t* arrived, hipStream_t s);
+hipError_t launch_masks_ge(int n, int64_t num_packets, uint64_t step, int dir,
+                           const GeParams& ge, uint8_t* state, uint8_t* arrived, hipStream_t s);
+hipError_t launch_aggregate(int gdtype, const AggParams& p, int64_t blocks, hipStream_t s);
+hipError_t launch_shard_step(int64_t d, const OptParams& o, float* theta, float* m, float* v,
+                             const float* g_hat, hipStream_t s);
+hipError_t launch_broadcast(int rdtype, const BcastParams& p, int64_t blocks, hipStream_t s);
+hipError_t launch_drift(int rdtype, const DriftParams& p, int64_t blocks, int n, int64_t d,
+                        int have_master, DriftOut* out, hipStream_t s);
+hipError_t launch_fused(int gdtype, int rdtype, const FusedParams& p, int64_t blocks,
+                        DriftOut* drift, hipStream_t s);
+hipError_t launch_drift_zero(DriftOut* out, hipStream_t s);
+
+}  // namespace lossy

@@ -1,0 +1,464 @@
+// HIP kernels of the lossy step for gfx950 and their launchers.
+//
+// Work decomposition shared by every per-packet kernel: one workgroup of 256
+// threads (4 wave64s) owns a chunk of up to 2048 consecutive elements of one
+// packet; thread t owns elements [8t, 8t + 8) of the chunk, so each row read
+// or written is one 16-byte (bf16) or two 16-byte (fp32) accesses per thread
+// and a wavefront touches 1 KiB (bf16) or 2 KiB (fp32) of contiguous HBM.
+// The masks of the packet sit in LDS as 64-bit words; loops over arrived or
+// stale rows walk the set bits with scalar (wave-uniform) control flow, so
+// a lost packet costs no memory traffic and causes no divergence.
+#include "kernels.h"
+
+#include <math.h>
+
+namespace lossy {
+
+// ---------------------------------------------------------------------------
+// Masks
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kThreads) void k_masks_bernoulli(int n, int64_t num_packets,
+                                                              uint64_t step, uint64_t dir,
+                                                              uint64_t seed, uint64_t thr,
+                                                              uint8_t* arrived) {
+    const int64_t total = (int64_t)n * num_packets;
+    for (int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x; idx < total;
+         idx += (int64_t)gridDim.x * kThreads) {
+        const int64_t i = idx / num_packets;
+        const int64_t k = idx - i * num_packets;
+        arrived[idx] = bernoulli_arrived((uint64_t)k, (uint64_t)i, step, dir, seed, thr) ? 1 : 0;
+    }
+}
+
+// Gilbert-Elliott masks: one workgroup per worker.  The chain's per-packet
+// transition is a map on {Good, Bad}, encoded in two bits (bit 0 = image of
+// Good, bit 1 = image of Bad).  Each thread composes the maps of a contiguous
+// run of packets, an exclusive scan of those composites across the
+// workgroup gives every run its starting state, and each thread then replays
+// its run, emitting arrivals.
+constexpr int kGeThreads = 1024;
+
+__device__ __forceinline__ uint32_t ge_apply(uint32_t map, uint32_t s) { return (map >> s) & 1u; }
+
+// (g after f)
+__device__ __forceinline__ uint32_t ge_compose(uint32_t g, uint32_t f) {
+    return ge_apply(g, ge_apply(f, 0)) | (ge_apply(g, ge_apply(f, 1)) << 1);
+}
+
+__global__ __launch_bounds__(kGeThreads) void k_masks_ge(int n, int64_t num_packets,
+                                                         uint64_t step, uint64_t dir,
+                                                         GeParams ge, uint8_t* state,
+                                                         uint8_t* arrived) {
+    __shared__ uint32_t s_map[kGeThreads];
+    const int i = blockIdx.x;
+    const int64_t per = (num_packets + kGeThreads - 1) / kGeThreads;
+    const int64_t k0 = (int64_t)threadIdx.x * per;
+    const int64_t k1 = k0 + per < num_packets ? k0 + per : num_packets;
+
+    uint32_t f = 0x2u;  // identity: Good -> Good, Bad -> Bad
+    for (int64_t k = k0; k < k1; ++k) {
+        uint64_t w0, w1;
+        philox4x64_10((uint64_t)k, (uint64_t)i, step, dir, ge.seed, 0, w0, w1);
+        const uint64_t u0 = w0 >> 32;
+        const uint32_t mk = (u0 < ge.thr_gb ? 1u : 0u) | ((u0 < ge.thr_bg ? 0u : 1u) << 1);
+        f = ge_compose(mk, f);
+    }
+    s_map[threadIdx.x] = f;
+    __syncthreads();
+    // Inclusive Hillis-Steele scan: s_map[t] = f_t o ... o f_0.
+    for (int off = 1; off < kGeThreads; off <<= 1) {
+        const uint32_t mine = s_map[threadIdx.x];
+        const uint32_t before = threadIdx.x >= off ? s_map[threadIdx.x - off] : 0x2u;
+        __syncthreads();
+        s_map[threadIdx.x] = ge_compose(mine, before);
+        __syncthreads();
+    }
+    const uint32_t s_in = state[i] ? 1u : 0u;
+    uint32_t s = threadIdx.x == 0 ? s_in : ge_apply(s_map[threadIdx.x - 1], s_in);
+    for (int64_t k = k0; k < k1; ++k) {
+        uint64_t w0, w1;
+        philox4x64_10((uint64_t)k, (uint64_t)i, step, dir, ge.seed, 0, w0, w1);
+        const uint64_t u0 = w0 >> 32, u1 = w1 >> 32;
+        s = s == 0 ? (u0 < ge.thr_gb ? 1u : 0u) : (u0 < ge.thr_bg ? 0u : 1u);
+        const bool lost = u1 < (s ? ge.thr_loss_bad : ge.thr_loss_good);
+        arrived[(int64_t)i * num_packets + k] = lost ? 0 : 1;
+    }
+    __syncthreads();  // every thread has read state[i]
+    if (threadIdx.x == kGeThreads - 1) state[i] = (uint8_t)ge_apply(s_map[kGeThreads - 1], s_in);
+}
+
+// ---------------------------------------------------------------------------
+// Per-packet chunk geometry
+// ---------------------------------------------------------------------------
+struct Chunk {
+    int64_t k;    // packet
+    int c;        // chunk within the packet
+    int64_t e0;   // first element of this thread
+    int nv;       // valid elements of this thread (0..8)
+};
+
+__device__ __forceinline__ Chunk chunk_of(int64_t d, int64_t L, int cpp) {
+    Chunk ch;
+    const int64_t b = blockIdx.x;
+    ch.k = b / cpp;
+    ch.c = (int)(b - ch.k * cpp);
+    const int64_t pk0 = ch.k * L;
+    const int64_t pend = pk0 + L < d ? pk0 + L : d;
+    ch.e0 = pk0 + (int64_t)ch.c * kChunk + (int64_t)threadIdx.x * kElems;
+    const int64_t rem = pend - ch.e0;
+    ch.nv = rem <= 0 ? 0 : (rem >= 8 ? 8 : (int)rem);
+    return ch;
+}
+
+// ---------------------------------------------------------------------------
+// One-stage entry points
+// ---------------------------------------------------------------------------
+template <class G>
+__global__ __launch_bounds__(kThreads) void k_aggregate(AggParams p) {
+    __shared__ uint64_t s_words[1][kMaxWords];
+    const Chunk ch = chunk_of(p.d, p.L, p.cpp);
+    MaskSource src{false, 0, 0, p.arrived};
+    const int dirs[1] = {0};
+    stage_masks(1, &src, p.n, p.P, ch.k, 0, dirs, s_words);
+    const int nw = (p.n + 63) >> 6;
+    const int K = popcount_words(s_words[0], nw);
+    if (ch.c == 0 && threadIdx.x == 0 && p.counts) p.counts[ch.k] = K;
+    if (ch.nv == 0) return;
+    float th[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    if (K == 0 && p.lam != 0.0f) load_f32x8(p.theta + ch.e0, ch.nv, th);
+    float g[8];
+    aggregate8<G>(reinterpret_cast<const typename G::T*>(p.grads), p.ld, ch.e0, ch.nv,
+                  s_words[0], nw, K, p.lam, th, g);
+    store_f32x8(p.g_hat + ch.e0, ch.nv, g);
+}
+
+__global__ __launch_bounds__(kThreads) void k_shard_step(int64_t d, OptParams o, float* theta,
+                                                         float* m, float* v,
+                                                         const float* g_hat) {
+    const int64_t e0 = ((int64_t)blockIdx.x * kThreads + threadIdx.x) * kElems;
+    if (e0 >= d) return;
+    const int nv = d - e0 >= 8 ? 8 : (int)(d - e0);
+    float th[8], mm[8], vv[8], g[8];
+    load_f32x8(theta + e0, nv, th);
+    load_f32x8(g_hat + e0, nv, g);
+    if (o.kind >= 1) load_f32x8(m + e0, nv, mm);
+    if (o.kind == 2) load_f32x8(v + e0, nv, vv);
+    update8(o, th, mm, vv, g);
+    store_f32x8(theta + e0, nv, th);
+    if (o.kind >= 1) store_f32x8(m + e0, nv, mm);
+    if (o.kind == 2) store_f32x8(v + e0, nv, vv);
+}
+
+template <class R>
+__global__ __launch_bounds__(kThreads) void k_broadcast(BcastParams p) {
+    __shared__ uint64_t s_words[1][kMaxWords];
+    const Chunk ch = chunk_of(p.d, p.L, p.cpp);
+    MaskSource src{false, 0, 0, p.arrived};
+    const int dirs[1] = {1};
+    stage_masks(1, &src, p.n, p.P, ch.k, 0, dirs, s_words);
+    if (ch.nv == 0) return;
+    const int nw = (p.n + 63) >> 6;
+    float th[8];
+    load_f32x8(p.theta + ch.e0, ch.nv, th);
+    Packed8<R> r;
+    r.pack(th);
+    typename R::T* reps = reinterpret_cast<typename R::T*>(p.replicas);
+    for (int w = 0; w < nw; ++w) {
+        uint64_t bits = uniform64(s_words[0][w]);
+        while (bits) {
+            const int i = w * 64 + __builtin_ctzll(bits);
+            bits &= bits - 1;
+            r.store(reps + (int64_t)i * p.ld + ch.e0, ch.nv);
+        }
+    }
+}
+
+// Drift over all rows of the chunk (rows read in ascending order).
+template <class R>
+__global__ __launch_bounds__(kThreads) void k_drift(DriftParams p) {
+    __shared__ uint64_t s_words[1][kMaxWords];
+    const Chunk ch = chunk_of(p.d, p.L, p.cpp);
+    const int nw = (p.n + 63) >> 6;
+    uint32_t stale = 0;
+    if (p.arrived) {
+        MaskSource src{false, 0, 0, p.arrived};
+        const int dirs[1] = {1};
+        stage_masks(1, &src, p.n, p.P, ch.k, 0, dirs, s_words);
+        if (ch.c == 0) stale = (uint32_t)(p.n - popcount_words(s_words[0], nw));
+    }
+    const typename R::T* reps = reinterpret_cast<const typename R::T*>(p.replicas);
+    double pair = 0.0, range = 0.0, abs_sum = 0.0;
+    if (ch.nv > 0) {
+        float r[8];
+        if (p.theta) {
+            float th[8];
+            load_f32x8(p.theta + ch.e0, ch.nv, th);
+            Packed8<R> pr;
+            pr.pack(th);
+#pragma unroll
+            for (int j = 0; j < 8; ++j) r[j] = pr.value(j);
+        } else {
+            load8<R>(reps + ch.e0, ch.nv, r);
+        }
+        Drift8 acc;
+        acc.init(false, r);
+        for (int i0 = 0; i0 < p.n; i0 += kBatch) {
+            float x[kBatch][8];
+#pragma unroll
+            for (int u = 0; u < kBatch; ++u) {
+                const int row = i0 + u < p.n ? i0 + u : i0;
+                load8<R>(reps + (int64_t)row * p.ld + ch.e0, ch.nv, x[u]);
+            }
+#pragma unroll
+            for (int u = 0; u < kBatch; ++u)
+                if (i0 + u < p.n) acc.add(x[u], r, ch.nv);
+        }
+        acc.finish(p.n, ch.nv, pair, range);
+        abs_sum = acc.abs_sum;
+    }
+    block_reduce_partial(pair, abs_sum, range, stale, 0, p.partials + blockIdx.x);
+}
+
+// Fixed-order reduction of the partials into the ll_drift record.
+constexpr int kFinalThreads = 1024;
+
+__global__ __launch_bounds__(kFinalThreads) void k_drift_final(const DriftPartial* parts,
+                                                               int64_t count, int n, int64_t d,
+                                                               int have_master, DriftOut* out) {
+    __shared__ double s_pair[kFinalThreads], s_abs[kFinalThreads], s_rng[kFinalThreads];
+    __shared__ unsigned long long s_stale[kFinalThreads], s_empty[kFinalThreads];
+    double pair = 0.0, a = 0.0, rg = 0.0;
+    unsigned long long st = 0, em = 0;
+    for (int64_t j = threadIdx.x; j < count; j += kFinalThreads) {
+        const DriftPartial q = parts[j];
+        pair += q.pair;
+        a += q.abs_sum;
+        rg = q.range > rg ? q.range : rg;
+        st += q.stale;
+        em += q.empty;
+    }
+    s_pair[threadIdx.x] = pair;
+    s_abs[threadIdx.x] = a;
+    s_rng[threadIdx.x] = rg;
+    s_stale[threadIdx.x] = st;
+    s_empty[threadIdx.x] = em;
+    __syncthreads();
+    for (int off = kFinalThreads / 2; off > 0; off >>= 1) {
+        if (threadIdx.x < off) {
+            s_pair[threadIdx.x] += s_pair[threadIdx.x + off];
+            s_abs[threadIdx.x] += s_abs[threadIdx.x + off];
+            const double o = s_rng[threadIdx.x + off];
+            s_rng[threadIdx.x] = o > s_rng[threadIdx.x] ? o : s_rng[threadIdx.x];
+            s_stale[threadIdx.x] += s_stale[threadIdx.x + off];
+            s_empty[threadIdx.x] += s_empty[threadIdx.x + off];
+        }
+        __syncthreads();
+    }
+    if (threadIdx.x == 0) {
+        const double pairs = (double)n * (double)(n - 1) * 0.5;
+        const double denom = (double)d * pairs;
+        DriftOut r;
+        r.max_abs = s_rng[0];
+        r.mean_sq = denom > 0.0 ? s_pair[0] / denom : 0.0;
+        r.rms = sqrt(r.mean_sq);
+        r.mean_abs_to_master =
+            have_master ? (d > 0 ? s_abs[0] / ((double)n * (double)d) : 0.0) : (double)NAN;
+        r.stale_packets = s_stale[0];
+        r.empty_packets = s_empty[0];
+        *out = r;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// The fused step: masks, aggregate, update, broadcast and drift partials in
+// one pass.  HBM traffic per packet: the arrived gradient rows (read once),
+// theta/m/v (read and written once), the arrived replica rows (written
+// once) and, with drift, the stale replica rows (read once).
+// ---------------------------------------------------------------------------
+template <class G, class R, bool DRIFT>
+__global__ __launch_bounds__(kThreads) void k_step_fused(FusedParams p) {
+    __shared__ uint64_t s_words[2][kMaxWords];
+    const Chunk ch = chunk_of(p.d, p.L, p.cpp);
+    const int dirs[2] = {0, 1};
+    stage_masks(2, p.src, p.n, p.P, ch.k, p.step, dirs, s_words);
+    const int nw = (p.n + 63) >> 6;
+    const int K = popcount_words(s_words[0], nw);
+    const int RC = popcount_words(s_words[1], nw);
+
+    if (ch.c == 0) {
+        if (threadIdx.x == 0 && p.counts) p.counts[ch.k] = K;
+        for (int i = threadIdx.x; i < p.n; i += kThreads) {
+            if (p.out_g) p.out_g[(int64_t)i * p.P + ch.k] = (s_words[0][i >> 6] >> (i & 63)) & 1;
+            if (p.out_b) p.out_b[(int64_t)i * p.P + ch.k] = (s_words[1][i >> 6] >> (i & 63)) & 1;
+        }
+    }
+
+    double pair = 0.0, range = 0.0, abs_sum = 0.0;
+    if (ch.nv > 0) {
+        float th[8], mm[8], vv[8], g[8];
+        load_f32x8(p.theta + ch.e0, ch.nv, th);
+        if (p.opt.kind >= 1) load_f32x8(p.m + ch.e0, ch.nv, mm);
+        if (p.opt.kind == 2) load_f32x8(p.v + ch.e0, ch.nv, vv);
+        aggregate8<G>(reinterpret_cast<const typename G::T*>(p.grads), p.ld_g, ch.e0, ch.nv,
+                      s_words[0], nw, K, p.lam, th, g);
+        update8(p.opt, th, mm, vv, g);
+        store_f32x8(p.theta + ch.e0, ch.nv, th);
+        if (p.opt.kind >= 1) store_f32x8(p.m + ch.e0, ch.nv, mm);
+        if (p.opt.kind == 2) store_f32x8(p.v + ch.e0, ch.nv, vv);
+
+        Packed8<R> r;
+        r.pack(th);
+        typename R::T* reps = reinterpret_cast<typename R::T*>(p.replicas);
+        Drift8 acc;
+        float rv[8];
+        if (DRIFT) {
+#pragma unroll
+            for (int j = 0; j < 8; ++j) rv[j] = r.value(j);
+            acc.init(RC > 0, rv);
+        }
+        const int last_bits = p.n - (nw - 1) * 64;
+        for (int w = 0; w < nw; ++w) {
+            const uint64_t valid = (w == nw - 1 && last_bits < 64) ? ((1ull << last_bits) - 1) : ~0ull;
+            const uint64_t bm = uniform64(s_words[1][w]);
+            uint64_t bits = bm & valid;
+            while (bits) {
+                const int i = w * 64 + __builtin_ctzll(bits);
+                bits &= bits - 1;
+                r.store(reps + (int64_t)i * p.ld_r + ch.e0, ch.nv);
+            }
+            if (DRIFT) {
+                uint64_t sb = ~bm & valid;
+                while (sb) {
+                    int idx[kBatch];
+#pragma unroll
+                    for (int u = 0; u < kBatch; ++u) {
+                        idx[u] = sb ? (w * 64 + __builtin_ctzll(sb)) : -1;
+                        sb &= sb - 1;
+                    }
+                    float x[kBatch][8];
+#pragma unroll
+                    for (int u = 0; u < kBatch; ++u) {
+                        const int row = idx[u] >= 0 ? idx[u] : idx[0];
+                        load8<R>(reps + (int64_t)row * p.ld_r + ch.e0, ch.nv, x[u]);
+                    }
+#pragma unroll
+                    for (int u = 0; u < kBatch; ++u)
+                        if (idx[u] >= 0) acc.add(x[u], rv, ch.nv);
+                }
+            }
+        }
+        if (DRIFT) {
+            acc.finish(p.n, ch.nv, pair, range);
+            abs_sum = acc.abs_sum;
+        }
+    }
+    if (DRIFT) {
+        const uint32_t stale = ch.c == 0 ? (uint32_t)(p.n - RC) : 0u;
+        const uint32_t empty = (ch.c == 0 && K == 0) ? 1u : 0u;
+        block_reduce_partial(pair, abs_sum, range, stale, empty, p.partials + blockIdx.x);
+    }
+}
+
+__global__ void k_drift_zero(DriftOut* out) {
+    if (threadIdx.x == 0) {
+        DriftOut r;
+        r.max_abs = 0.0;
+        r.mean_sq = 0.0;
+        r.rms = 0.0;
+        r.mean_abs_to_master = 0.0;
+        r.stale_packets = 0;
+        r.empty_packets = 0;
+        *out = r;
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Launchers (host)
+// ---------------------------------------------------------------------------
+static int64_t grid_cap(int64_t blocks) { return blocks < (1ll << 20) ? blocks : (1ll << 20); }
+
+hipError_t launch_masks_bernoulli(int n, int64_t num_packets, uint64_t step, int dir,
+                                  uint64_t seed, uint64_t thr, uint8_t* arrived,
+                                  hipStream_t s) {
+    const int64_t total = (int64_t)n * num_packets;
+    const int64_t blocks = grid_cap((total + kThreads - 1) / kThreads);
+    hipLaunchKernelGGL(k_masks_bernoulli, dim3((unsigned)blocks), dim3(kThreads), 0, s, n,
+                       num_packets, step, (uint64_t)dir, seed, thr, arrived);
+    return hipGetLastError();
+}
+
+hipError_t launch_masks_ge(int n, int64_t num_packets, uint64_t step, int dir,
+                           const GeParams& ge, uint8_t* state, uint8_t* arrived,
+                           hipStream_t s) {
+    hipLaunchKernelGGL(k_masks_ge, dim3((unsigned)n), dim3(kGeThreads), 0, s, n, num_packets,
+                       step, (uint64_t)dir, ge, state, arrived);
+    return hipGetLastError();
+}
+
+hipError_t launch_aggregate(int gdtype, const AggParams& p, int64_t blocks, hipStream_t s) {
+    if (gdtype == 1)
+        hipLaunchKernelGGL(k_aggregate<BF16>, dim3((unsigned)blocks), dim3(kThreads), 0, s, p);
+    else
+        hipLaunchKernelGGL(k_aggregate<F32>, dim3((unsigned)blocks), dim3(kThreads), 0, s, p);
+    return hipGetLastError();
+}
+
+hipError_t launch_shard_step(int64_t d, const OptParams& o, float* theta, float* m, float* v,
+                             const float* g_hat, hipStream_t s) {
+    const int64_t blocks = (d + kChunk - 1) / kChunk;
+    hipLaunchKernelGGL(k_shard_step, dim3((unsigned)blocks), dim3(kThreads), 0, s, d, o, theta,
+                       m, v, g_hat);
+    return hipGetLastError();
+}
+
+hipError_t launch_broadcast(int rdtype, const BcastParams& p, int64_t blocks, hipStream_t s) {
+    if (rdtype == 1)
+        hipLaunchKernelGGL(k_broadcast<BF16>, dim3((unsigned)blocks), dim3(kThreads), 0, s, p);
+    else
+        hipLaunchKernelGGL(k_broadcast<F32>, dim3((unsigned)blocks), dim3(kThreads), 0, s, p);
+    return hipGetLastError();
+}
+
+hipError_t launch_drift(int rdtype, const DriftParams& p, int64_t blocks, int n, int64_t d,
+                        int have_master, DriftOut* out, hipStream_t s) {
+    if (rdtype == 1)
+        hipLaunchKernelGGL(k_drift<BF16>, dim3((unsigned)blocks), dim3(kThreads), 0, s, p);
+    else
+        hipLaunchKernelGGL(k_drift<F32>, dim3((unsigned)blocks), dim3(kThreads), 0, s, p);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_drift_final, dim3(1), dim3(kFinalThreads), 0, s, p.partials, blocks, n,
+                       d, have_master, out);
+    return hipGetLastError();
+}
+
+template <class G, class R>
+static void launch_fused_gr(bool drift, const FusedParams& p, int64_t blocks, hipStream_t s) {
+    if (drift)
+        hipLaunchKernelGGL((k_step_fused<G, R, true>), dim3((unsigned)blocks), dim3(kThreads), 0,
+                           s, p);
+    else
+        hipLaunchKernelGGL((k_step_fused<G, R, false>), dim3((unsigned)blocks), dim3(kThreads), 0,
+                           s, p);
+}
+
+hipError_t launch_fused(int gdtype, int rdtype, const FusedParams& p, int64_t blocks,
+                        DriftOut* drift, hipStream_t s) {
+    const bool dr = drift != nullptr;
+    if (gdtype == 1 && rdtype == 1) launch_fused_gr<BF16, BF16>(dr, p, blocks, s);
+    else if (gdtype == 1) launch_fused_gr<BF16, F32>(dr, p, blocks, s);
+    else if (rdtype == 1) launch_fused_gr<F32, BF16>(dr, p, blocks, s);
+    else launch_fused_gr<F32, F32>(dr, p, blocks, s);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess || !dr) return e;
+    hipLaunchKernelGGL(k_drift_final, dim3(1), dim3(kFinalThreads), 0, s, p.partials, blocks,
+                       p.n, p.d, 1, drift);
+    return hipGetLastError();
+}
+
+hipError_t launch_drift_zero(DriftOut* out, hipStream_t s) {
+    hipLaunchKernelGGL(k_drift_zero, dim3(1), dim3(64), 0, s, out);
+    return hipGetLastError();
+}
+
+}  // namespace lossy

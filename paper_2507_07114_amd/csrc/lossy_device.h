@@ -1,0 +1,397 @@
+// Device-side building blocks of the lossy step for gfx950 (CDNA4, wave64).
+//
+// Every kernel of the library is assembled from the pieces in this header,
+// so the fused step and the one-stage-at-a-time entry points run the same
+// arithmetic in the same order and produce bit-identical results.  The
+// library is compiled with -ffp-contract=off: every fused multiply-add below
+// is written out explicitly.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace lossy {
+
+constexpr int kThreads = 256;              // threads per workgroup (4 waves)
+constexpr int kElems = 8;                  // consecutive elements per thread
+constexpr int kChunk = kThreads * kElems;  // elements per workgroup
+constexpr int kMaxWorkers = 1024;
+constexpr int kMaxWords = kMaxWorkers / 64;
+constexpr int kBatch = 8;                  // rows in flight per thread
+
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+// ---------------------------------------------------------------------------
+// Philox4x64-10 (Salmon, Moraes, Dror, Shaw, SC'11): ten rounds, each
+// multiplying words 0 and 2 by fixed odd constants, exchanging the halves of
+// the products with words 1 and 3 and the round key; the key is bumped by two
+// Weyl constants between rounds.  Only output words 0 and 1 are needed.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ void philox4x64_10(uint64_t c0, uint64_t c1, uint64_t c2,
+                                              uint64_t c3, uint64_t k0, uint64_t k1,
+                                              uint64_t& w0, uint64_t& w1) {
+    const uint64_t kM0 = 0xD2E7470EE14C6C93ull, kM1 = 0xCA5A826395121157ull;
+    const uint64_t kW0 = 0x9E3779B97F4A7C15ull, kW1 = 0xBB67AE8584CAA73Bull;
+#pragma unroll
+    for (int r = 0; r < 10; ++r) {
+        if (r) {
+            k0 += kW0;
+            k1 += kW1;
+        }
+        const uint64_t hi0 = __umul64hi(kM0, c0), lo0 = kM0 * c0;
+        const uint64_t hi1 = __umul64hi(kM1, c2), lo1 = kM1 * c2;
+        const uint64_t n0 = hi1 ^ c1 ^ k0;
+        const uint64_t n2 = hi0 ^ c3 ^ k1;
+        c0 = n0;
+        c1 = lo1;
+        c2 = n2;
+        c3 = lo0;
+    }
+    w0 = c0;
+    w1 = c1;
+}
+
+// Arrival of (packet k, worker i, step t, direction dir) under i.i.d. loss:
+// lost iff hi32(w0) < thr, thr = ceil(p * 2^32) (host-computed).
+__device__ __forceinline__ bool bernoulli_arrived(uint64_t k, uint64_t i, uint64_t t,
+                                                  uint64_t dir, uint64_t seed,
+                                                  uint64_t thr) {
+    uint64_t w0, w1;
+    philox4x64_10(k, i, t, dir, seed, 0, w0, w1);
+    return (w0 >> 32) >= thr;
+}
+
+// ---------------------------------------------------------------------------
+// Element types.  bf16 is carried as its 16-bit pattern (the upper half of a
+// binary32); narrowing rounds to nearest even, NaN stays quiet NaN.
+// ---------------------------------------------------------------------------
+struct F32 {
+    typedef float T;
+};
+struct BF16 {
+    typedef uint16_t T;
+};
+
+__device__ __forceinline__ float bf16_to_f32(uint32_t h) { return __uint_as_float(h << 16); }
+
+__device__ __forceinline__ uint32_t f32_to_bf16(float f) {
+    const uint32_t u = __float_as_uint(f);
+    if ((u & 0x7FFFFFFFu) > 0x7F800000u) return (u >> 16) | 0x40u;
+    return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
+}
+
+// Load 8 consecutive elements (16-byte aligned when full) as floats.
+template <class E>
+__device__ __forceinline__ void load8(const typename E::T* p, int nv, float (&x)[8]);
+
+template <>
+__device__ __forceinline__ void load8<F32>(const float* p, int nv, float (&x)[8]) {
+    if (nv == 8) {
+        const u32x4 a = *reinterpret_cast<const u32x4*>(p);
+        const u32x4 b = *reinterpret_cast<const u32x4*>(p + 4);
+        x[0] = __uint_as_float(a.x); x[1] = __uint_as_float(a.y);
+        x[2] = __uint_as_float(a.z); x[3] = __uint_as_float(a.w);
+        x[4] = __uint_as_float(b.x); x[5] = __uint_as_float(b.y);
+        x[6] = __uint_as_float(b.z); x[7] = __uint_as_float(b.w);
+    } else {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) x[j] = j < nv ? p[j] : 0.0f;
+    }
+}
+
+template <>
+__device__ __forceinline__ void load8<BF16>(const uint16_t* p, int nv, float (&x)[8]) {
+    if (nv == 8) {
+        const u32x4 a = *reinterpret_cast<const u32x4*>(p);
+        x[0] = bf16_to_f32(a.x & 0xFFFFu); x[1] = bf16_to_f32(a.x >> 16);
+        x[2] = bf16_to_f32(a.y & 0xFFFFu); x[3] = bf16_to_f32(a.y >> 16);
+        x[4] = bf16_to_f32(a.z & 0xFFFFu); x[5] = bf16_to_f32(a.z >> 16);
+        x[6] = bf16_to_f32(a.w & 0xFFFFu); x[7] = bf16_to_f32(a.w >> 16);
+    } else {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) x[j] = j < nv ? bf16_to_f32(p[j]) : 0.0f;
+    }
+}
+
+// Rounded storage form of 8 values (what a replica row holds).
+template <class E>
+struct Packed8;
+
+template <>
+struct Packed8<F32> {
+    u32x4 a, b;
+    __device__ __forceinline__ void pack(const float (&x)[8]) {
+        a = u32x4{__float_as_uint(x[0]), __float_as_uint(x[1]), __float_as_uint(x[2]),
+                  __float_as_uint(x[3])};
+        b = u32x4{__float_as_uint(x[4]), __float_as_uint(x[5]), __float_as_uint(x[6]),
+                  __float_as_uint(x[7])};
+    }
+    __device__ __forceinline__ float value(int j) const {
+        const u32x4& h = j < 4 ? a : b;
+        const int q = j & 3;
+        return __uint_as_float(q == 0 ? h.x : q == 1 ? h.y : q == 2 ? h.z : h.w);
+    }
+    __device__ __forceinline__ void store(float* p, int nv) const {
+        if (nv == 8) {
+            __builtin_nontemporal_store(a, reinterpret_cast<u32x4*>(p));
+            __builtin_nontemporal_store(b, reinterpret_cast<u32x4*>(p + 4));
+        } else {
+            for (int j = 0; j < nv; ++j) p[j] = value(j);
+        }
+    }
+};
+
+template <>
+struct Packed8<BF16> {
+    u32x4 a;
+    __device__ __forceinline__ void pack(const float (&x)[8]) {
+        a = u32x4{f32_to_bf16(x[0]) | (f32_to_bf16(x[1]) << 16),
+                  f32_to_bf16(x[2]) | (f32_to_bf16(x[3]) << 16),
+                  f32_to_bf16(x[4]) | (f32_to_bf16(x[5]) << 16),
+                  f32_to_bf16(x[6]) | (f32_to_bf16(x[7]) << 16)};
+    }
+    __device__ __forceinline__ float value(int j) const {
+        const int q = j >> 1;
+        const uint32_t w = q == 0 ? a.x : q == 1 ? a.y : q == 2 ? a.z : a.w;
+        return bf16_to_f32((j & 1) ? (w >> 16) : (w & 0xFFFFu));
+    }
+    __device__ __forceinline__ void store(uint16_t* p, int nv) const {
+        if (nv == 8) {
+            __builtin_nontemporal_store(a, reinterpret_cast<u32x4*>(p));
+        } else {
+            for (int j = 0; j < nv; ++j) p[j] = (uint16_t)f32_to_bf16(value(j));
+        }
+    }
+};
+
+__device__ __forceinline__ void load_f32x8(const float* p, int nv, float (&x)[8]) {
+    load8<F32>(p, nv, x);
+}
+
+__device__ __forceinline__ void store_f32x8(float* p, int nv, const float (&x)[8]) {
+    if (nv == 8) {
+        *reinterpret_cast<u32x4*>(p) = u32x4{__float_as_uint(x[0]), __float_as_uint(x[1]),
+                                             __float_as_uint(x[2]), __float_as_uint(x[3])};
+        *reinterpret_cast<u32x4*>(p + 4) = u32x4{__float_as_uint(x[4]), __float_as_uint(x[5]),
+                                                 __float_as_uint(x[6]), __float_as_uint(x[7])};
+    } else {
+        for (int j = 0; j < nv; ++j) p[j] = x[j];
+    }
+}
+
+// Wave-uniform copy of a 64-bit value held identically by all active lanes.
+__device__ __forceinline__ uint64_t uniform64(uint64_t x) {
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)x);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)(x >> 32));
+    return ((uint64_t)hi << 32) | lo;
+}
+
+// ---------------------------------------------------------------------------
+// Per-packet masks in LDS: word w bit b = arrival of worker 64 w + b.
+// ---------------------------------------------------------------------------
+struct MaskSource {
+    // draw == true: Bernoulli draw in the kernel with (seed, thr);
+    // otherwise read bytes from mem[i * num_packets + k].
+    bool draw;
+    uint64_t seed, thr;
+    const uint8_t* mem;
+};
+
+// Stage the masks of packet k for `ndir` directions into words[dir][w].
+// All threads of the workgroup must call it (it ends with a barrier).
+__device__ __forceinline__ void stage_masks(int ndir, const MaskSource* src, int n,
+                                            int64_t num_packets, int64_t k, uint64_t step,
+                                            const int* dirs,
+                                            uint64_t (*words)[kMaxWords]) {
+    const int nw = (n + 63) >> 6;
+    const int span = nw * 64;
+    for (int idx = threadIdx.x; idx < ndir * span; idx += kThreads) {
+        const int s = idx / span;
+        const int i = idx - s * span;
+        bool arrived = false;
+        if (i < n) {
+            if (src[s].draw)
+                arrived = bernoulli_arrived((uint64_t)k, (uint64_t)i, step, (uint64_t)dirs[s],
+                                            src[s].seed, src[s].thr);
+            else
+                arrived = src[s].mem[(int64_t)i * num_packets + k] != 0;
+        }
+        const uint64_t word = __ballot(arrived);
+        if ((threadIdx.x & 63) == 0) words[s][i >> 6] = word;
+    }
+    __syncthreads();
+}
+
+__device__ __forceinline__ int popcount_words(const uint64_t* words, int nw) {
+    int c = 0;
+    for (int w = 0; w < nw; ++w) c += __popcll(uniform64(words[w]));
+    return c;
+}
+
+// ---------------------------------------------------------------------------
+// Aggregate (Section 3 step (2)): g[j] = sum over arrived rows, ascending, of
+// grads[i][e0 + j], divided by K; lam * theta when K = 0.
+// ---------------------------------------------------------------------------
+template <class E>
+__device__ __forceinline__ void aggregate8(const typename E::T* grads, int64_t ld,
+                                           int64_t e0, int nv, const uint64_t* gm, int nw,
+                                           int K, float lam, const float (&th)[8],
+                                           float (&g)[8]) {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) g[j] = 0.0f;
+    for (int w = 0; w < nw; ++w) {
+        uint64_t bits = uniform64(gm[w]);
+        while (bits) {
+            int idx[kBatch];
+#pragma unroll
+            for (int u = 0; u < kBatch; ++u) {
+                idx[u] = bits ? (w * 64 + __builtin_ctzll(bits)) : -1;
+                bits &= bits - 1;  // no-op once bits == 0
+            }
+            float x[kBatch][8];
+#pragma unroll
+            for (int u = 0; u < kBatch; ++u) {
+                const int row = idx[u] >= 0 ? idx[u] : idx[0];
+                load8<E>(grads + (int64_t)row * ld + e0, nv, x[u]);
+            }
+#pragma unroll
+            for (int u = 0; u < kBatch; ++u) {
+                if (idx[u] >= 0) {
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) g[j] += x[u][j];
+                }
+            }
+        }
+    }
+    if (K > 0) {
+        const float kf = (float)K;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) g[j] = g[j] / kf;
+    } else {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) g[j] = lam * th[j];
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Owner update (Section 3 step (3)), 8 elements, fp32.
+// ---------------------------------------------------------------------------
+struct OptParams {
+    int kind;  // 0 SGD, 1 momentum, 2 Adam
+    float lr, momentum, beta1, beta2, eps;
+    float bc1, bc2;  // 1 - beta^(t+1), rounded to fp32 on the host
+};
+
+__device__ __forceinline__ void update8(const OptParams& o, float (&th)[8], float (&m)[8],
+                                        float (&v)[8], const float (&g)[8]) {
+    if (o.kind == 0) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) th[j] = th[j] - o.lr * g[j];
+    } else if (o.kind == 1) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            m[j] = o.momentum * m[j] + g[j];
+            th[j] = th[j] - o.lr * m[j];
+        }
+    } else {
+        const float a1 = 1.0f - o.beta1, a2 = 1.0f - o.beta2;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            m[j] = o.beta1 * m[j] + a1 * g[j];
+            v[j] = o.beta2 * v[j] + a2 * (g[j] * g[j]);
+            const float mh = m[j] / o.bc1;
+            const float vh = v[j] / o.bc2;
+            th[j] = th[j] - o.lr * (mh / (sqrtf(vh) + o.eps));
+        }
+    }
+}
+
+// ---------------------------------------------------------------------------
+// Drift accumulation for the 8 elements of one thread.  Values are compared
+// with the reference r = c(theta) of the element: d = x - r in fp64.
+// ---------------------------------------------------------------------------
+struct Drift8 {
+    double s1[8], s2[8];
+    float hi[8], lo[8];
+    double abs_sum;
+
+    __device__ __forceinline__ void init(bool any_equal_ref, const float (&r)[8]) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            s1[j] = 0.0;
+            s2[j] = 0.0;
+            hi[j] = any_equal_ref ? r[j] : -__builtin_inff();
+            lo[j] = any_equal_ref ? r[j] : __builtin_inff();
+        }
+        abs_sum = 0.0;
+    }
+    __device__ __forceinline__ void add(const float (&x)[8], const float (&r)[8], int nv) {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            if (j < nv) {
+                const double d = (double)x[j] - (double)r[j];
+                s1[j] = s1[j] + d;
+                s2[j] = __fma_rn(d, d, s2[j]);
+                abs_sum = abs_sum + fabs(d);
+                hi[j] = fmaxf(hi[j], x[j]);
+                lo[j] = fminf(lo[j], x[j]);
+            }
+        }
+    }
+    // Fold into per-thread totals: pair sum N*S2 - S1^2 and max range.
+    __device__ __forceinline__ void finish(int n, int nv, double& pair, double& range) const {
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+            if (j < nv) {
+                const double ps = (double)n * s2[j] - s1[j] * s1[j];
+                pair = pair + (ps > 0.0 ? ps : 0.0);
+                const double rg = (double)hi[j] - (double)lo[j];
+                range = rg > range ? rg : range;
+            }
+        }
+    }
+};
+
+struct DriftPartial {
+    double pair, abs_sum, range;
+    uint32_t stale, empty;
+};
+
+// Fixed-order workgroup reduction of (pair, abs, range); thread 0 writes
+// the partial together with the packet bookkeeping counts.
+__device__ __forceinline__ void block_reduce_partial(double pair, double abs_sum,
+                                                     double range, uint32_t stale,
+                                                     uint32_t empty, DriftPartial* out) {
+    __shared__ double s_red[3][kThreads / 64];
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) {
+        pair += __shfl_down(pair, off, 64);
+        abs_sum += __shfl_down(abs_sum, off, 64);
+        const double r2 = __shfl_down(range, off, 64);
+        range = r2 > range ? r2 : range;
+    }
+    const int wave = threadIdx.x >> 6;
+    if ((threadIdx.x & 63) == 0) {
+        s_red[0][wave] = pair;
+        s_red[1][wave] = abs_sum;
+        s_red[2][wave] = range;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        double p = 0.0, a = 0.0, r = 0.0;
+        for (int w = 0; w < kThreads / 64; ++w) {
+            p += s_red[0][w];
+            a += s_red[1][w];
+            r = s_red[2][w] > r ? s_red[2][w] : r;
+        }
+        DriftPartial dp;
+        dp.pair = p;
+        dp.abs_sum = a;
+        dp.range = r;
+        dp.stale = stale;
+        dp.empty = empty;
+        *out = dp;
+    }
+}
+
+}  // namespace lossy

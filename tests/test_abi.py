@@ -1,0 +1,112 @@
+"""The C ABI library loads and exports every declared entry point; argument
+validation rejects bad input before any device work (CPU only: no call
+here reaches a kernel launch)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2507_07114_amd as ll
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "lossy.h")
+
+
+def _declared():
+    text = open(HEADER).read()
+    return re.findall(r"^LL_API\s+[\w\s\*]*?\b(\w+)\s*\(", text, flags=re.M)
+
+
+def test_header_declares_the_boundary():
+    names = set(_declared())
+    assert names == {"ll_masks", "lossy_aggregate", "shard_step", "lossy_broadcast",
+                     "drift_stats", "lossy_step_fused", "ll_workspace_bytes", "ll_last_error"}
+
+
+def test_library_exports_every_declared_symbol():
+    assert os.path.exists(ll.library_path()), "run `python -m paper_2507_07114_amd.build`"
+    lib = ctypes.CDLL(ll.library_path())
+    for name in _declared():
+        assert hasattr(lib, name), name
+    # and the binding wraps each of them under the same name
+    for name in _declared():
+        assert callable(getattr(ll, name)), name
+
+
+def test_struct_layouts():
+    assert ctypes.sizeof(ll.LossSpec) == 56
+    assert ctypes.sizeof(ll.OptSpec) == 28
+
+
+def test_workspace_bytes_host_logic():
+    # partials: 32 B per workgroup (P * ceil(L / 2048)), then two n*P mask areas,
+    # each rounded up to 256 B.
+    def r256(x):
+        return (x + 255) // 256 * 256
+    n, d, L = 64, 105_250_000, 4096
+    P = (d + L - 1) // L
+    assert ll.ll_workspace_bytes(n, d, L) == r256(P * 2 * 32) + 2 * r256(n * P)
+    assert ll.ll_workspace_bytes(4, 10, 8) == 256 + 2 * 256
+    assert ll.ll_workspace_bytes(0, 10, 8) == 0      # invalid n
+    assert ll.ll_workspace_bytes(4, 10, 12) == 0     # packet not a multiple of 8
+    assert ll.ll_workspace_bytes(4, -1, 8) == 0
+
+
+def _raw():
+    return ctypes.CDLL(ll.library_path())
+
+
+@pytest.mark.parametrize("args,code,frag", [
+    ((0, 16, 8, 0, 16, 16, 0, 0.0, 0, 16, 0, 0), -1, "n=0"),
+    ((2000, 16, 8, 0, 16, 16, 0, 0.0, 0, 16, 0, 0), -1, "n=2000"),
+    ((2, -5, 8, 0, 16, 16, 16, 0.0, 0, 16, 0, 0), -1, "negative"),
+    ((2, 16, 12, 0, 16, 16, 16, 0.0, 0, 16, 0, 0), -1, "multiple of 8"),
+    ((2, 16, 8, 7, 16, 16, 16, 0.0, 0, 16, 0, 0), -1, "dtype"),
+    ((2, 16, 8, 0, 0, 16, 16, 0.0, 0, 16, 0, 0), -1, "grads is NULL"),
+    ((2, 16, 8, 0, 16, 8, 16, 0.0, 0, 16, 0, 0), -1, "ld=8 < d=16"),
+    ((2, 16, 8, 0, 16, 20, 16, 0.0, 0, 16, 0, 0), -2, "multiple of 8"),
+    ((2, 16, 8, 0, 18, 16, 16, 0.0, 0, 16, 0, 0), -2, "aligned"),
+    ((2, 16, 8, 0, 16, 16, 0, 0.0, 0, 16, 0, 0), -1, "arrived is NULL"),
+    ((2, 16, 8, 0, 16, 16, 16, 0.5, 0, 16, 0, 0), -1, "theta is NULL"),
+])
+def test_aggregate_rejects_bad_arguments(args, code, frag):
+    lib = _raw()
+    f = lib.lossy_aggregate
+    f.argtypes = [ctypes.c_int32, ctypes.c_int64, ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p,
+                  ctypes.c_int64, ctypes.c_void_p, ctypes.c_float, ctypes.c_void_p,
+                  ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+    assert f(*args) == code
+    lib.ll_last_error.restype = ctypes.c_char_p
+    assert frag in lib.ll_last_error().decode()
+
+
+def test_masks_and_opt_validation():
+    lib = _raw()
+    lib.ll_last_error.restype = ctypes.c_char_p
+    bad_p = ll.bernoulli(1.5)
+    fm = lib.ll_masks
+    fm.argtypes = [ctypes.c_int32, ctypes.c_int64, ctypes.c_uint64, ctypes.c_int32,
+                   ctypes.POINTER(ll.LossSpec), ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+    assert fm(4, 10, 0, 0, ctypes.byref(bad_p), None, 16, None) == -1
+    assert "p outside" in lib.ll_last_error().decode()
+    ge = ll.gilbert_elliott(0.1, 0.2, 0.0, 0.5)
+    assert fm(4, 10, 0, 0, ctypes.byref(ge), None, 16, None) == -1
+    assert "ge_state" in lib.ll_last_error().decode()
+    assert fm(4, 10, 0, 3, ctypes.byref(ll.bernoulli(0.1)), None, 16, None) == -1
+    # Zero packets is a valid no-op that touches no device.
+    assert fm(4, 0, 0, 0, ctypes.byref(ll.bernoulli(0.1)), None, 16, None) == 0
+
+    fs = lib.shard_step
+    fs.argtypes = [ctypes.POINTER(ll.OptSpec), ctypes.c_int64, ctypes.c_uint64, ctypes.c_void_p,
+                   ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+    adam = ll.adam(1e-3, 0.9, 0.95, 1e-8)
+    assert fs(ctypes.byref(adam), 16, 0, 16, 16, None, 16, None) == -1
+    assert "v is NULL" in lib.ll_last_error().decode()
+    mom = ll.sgd_momentum(1e-2, 0.9)
+    assert fs(ctypes.byref(mom), 16, 0, 16, None, None, 16, None) == -1
+    bad = ll.OptSpec(9, 0.1, 0, 0, 0, 0, 0)
+    assert fs(ctypes.byref(bad), 16, 0, 16, None, None, 16, None) == -1
+    assert "unknown optimizer" in lib.ll_last_error().decode()
+    # d = 0 returns before touching the device.
+    assert fs(ctypes.byref(ll.sgd(0.1)), 0, 0, 16, None, None, 16, None) == 0
