@@ -85,6 +85,29 @@ def read_pmc_traffic(expect_hash: str):
         return None
 
 
+def hbm_copy_probe(nbytes: int = 2 << 30, reps: int = 5) -> float:
+    """Device-to-device copy of a known size (torch's copy kernel): achievable
+    HBM bandwidth for a 50/50 read/write stream on this GPU, as context."""
+    import numpy as np
+    import torch
+    src = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    times = []
+    for _ in range(reps):
+        a = torch.cuda.Event(enable_timing=True)
+        b = torch.cuda.Event(enable_timing=True)
+        a.record()
+        dst.copy_(src)
+        b.record()
+        torch.cuda.synchronize()
+        times.append(a.elapsed_time(b))
+    del src, dst
+    torch.cuda.empty_cache()
+    return 2 * nbytes / (float(np.median(times)) * 1e-3) / 1e9
+
+
 def cpu_baseline(w, dev, packets_sample: int):
     """The oracle, as it stands, on a bounded sample of packets of the same
     workload (inputs copied from the device before any step runs)."""
@@ -162,6 +185,8 @@ def main():
     if w.loss["kind"] != wl.BERNOULLI:
         log("the benchmark times Bernoulli-loss workloads only")
         sys.exit(1)
+    copy_gbs = hbm_copy_probe()
+    log(f"plain 2 GiB device copy: {copy_gbs:.0f} GB/s")
     log(f"workload {name}: n={w.n} d={w.d} packet={w.packet} P={w.num_packets}")
     dev = DeviceState(w)
     torch.cuda.synchronize()
@@ -236,6 +261,7 @@ def main():
         "elements_per_s": round(w.n * w.d / (ms_per_step * 1e-3), 1),
         "shard_elements_per_s": round(w.d / (ms_per_step * 1e-3), 1),
         "algorithmic_bytes_per_step": mean_b,
+        "hbm_copy_probe_gbs": round(copy_gbs, 1),
         "roofline": {
             "bound": "hbm",
             "kernel": "k_step_fused (+ k_drift_final)",

@@ -202,15 +202,15 @@ __global__ __launch_bounds__(kThreads) void k_drift(DriftParams p) {
         }
         Drift8 acc;
         acc.init(false, r);
-        for (int i0 = 0; i0 < p.n; i0 += kBatch) {
-            float x[kBatch][8];
+        for (int i0 = 0; i0 < p.n; i0 += kBatchStale) {
+            float x[kBatchStale][8];
 #pragma unroll
-            for (int u = 0; u < kBatch; ++u) {
+            for (int u = 0; u < kBatchStale; ++u) {
                 const int row = i0 + u < p.n ? i0 + u : i0;
                 load8<R>(reps + (int64_t)row * p.ld + ch.e0, ch.nv, x[u]);
             }
 #pragma unroll
-            for (int u = 0; u < kBatch; ++u)
+            for (int u = 0; u < kBatchStale; ++u)
                 if (i0 + u < p.n) acc.add(x[u], r, ch.nv);
         }
         acc.finish(p.n, ch.nv, pair, range);
@@ -329,20 +329,20 @@ __global__ __launch_bounds__(kThreads) void k_step_fused(FusedParams p) {
             if (DRIFT) {
                 uint64_t sb = ~bm & valid;
                 while (sb) {
-                    int idx[kBatch];
+                    int idx[kBatchStale];
 #pragma unroll
-                    for (int u = 0; u < kBatch; ++u) {
+                    for (int u = 0; u < kBatchStale; ++u) {
                         idx[u] = sb ? (w * 64 + __builtin_ctzll(sb)) : -1;
                         sb &= sb - 1;
                     }
-                    float x[kBatch][8];
+                    float x[kBatchStale][8];
 #pragma unroll
-                    for (int u = 0; u < kBatch; ++u) {
+                    for (int u = 0; u < kBatchStale; ++u) {
                         const int row = idx[u] >= 0 ? idx[u] : idx[0];
                         load8<R>(reps + (int64_t)row * p.ld_r + ch.e0, ch.nv, x[u]);
                     }
 #pragma unroll
-                    for (int u = 0; u < kBatch; ++u)
+                    for (int u = 0; u < kBatchStale; ++u)
                         if (idx[u] >= 0) acc.add(x[u], rv, ch.nv);
                 }
             }

@@ -17,7 +17,8 @@ constexpr int kElems = 8;                  // consecutive elements per thread
 constexpr int kChunk = kThreads * kElems;  // elements per workgroup
 constexpr int kMaxWorkers = 1024;
 constexpr int kMaxWords = kMaxWorkers / 64;
-constexpr int kBatch = 8;                  // rows in flight per thread
+constexpr int kBatchGrad = 4;   // gradient rows in flight per thread (aggregate)
+constexpr int kBatchStale = 4;  // stale replica rows in flight per thread (drift)
 
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
@@ -242,20 +243,20 @@ __device__ __forceinline__ void aggregate8(const typename E::T* grads, int64_t l
     for (int w = 0; w < nw; ++w) {
         uint64_t bits = uniform64(gm[w]);
         while (bits) {
-            int idx[kBatch];
+            int idx[kBatchGrad];
 #pragma unroll
-            for (int u = 0; u < kBatch; ++u) {
+            for (int u = 0; u < kBatchGrad; ++u) {
                 idx[u] = bits ? (w * 64 + __builtin_ctzll(bits)) : -1;
                 bits &= bits - 1;  // no-op once bits == 0
             }
-            float x[kBatch][8];
+            float x[kBatchGrad][8];
 #pragma unroll
-            for (int u = 0; u < kBatch; ++u) {
+            for (int u = 0; u < kBatchGrad; ++u) {
                 const int row = idx[u] >= 0 ? idx[u] : idx[0];
                 load8<E>(grads + (int64_t)row * ld + e0, nv, x[u]);
             }
 #pragma unroll
-            for (int u = 0; u < kBatch; ++u) {
+            for (int u = 0; u < kBatchGrad; ++u) {
                 if (idx[u] >= 0) {
 #pragma unroll
                     for (int j = 0; j < 8; ++j) g[j] += x[u][j];
