@@ -93,9 +93,9 @@ typedef struct {
  *   LL_ADAM          m = beta1 m + (1-beta1) g;  v = beta2 v + (1-beta2) g^2;
  *                    theta -= lr * (m / (1-beta1^(t+1))) /
  *                             (sqrt(v / (1-beta2^(t+1))) + eps)
- * fallback_lambda: when no contribution of a packet arrived, the paper says
- * to fall back to a small regulariser ("Unbiased Gradient Aggregation");
- * the aggregate is then fallback_lambda * theta (0 gives g_hat = 0).
+ * fallback_lambda: for a packet with no arrived contribution the paper
+ * leaves the substitute open ("Unbiased Gradient Aggregation"); here the
+ * aggregate is then fallback_lambda * theta (0 gives g_hat = 0).
  */
 typedef struct {
     int32_t kind;

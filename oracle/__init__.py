@@ -5,7 +5,7 @@ what the paper "Distributed Training under Packet Loss" (Weintraub, Banner,
 Orda, 2025) defines for one owner's shard:
 
   * Section 3 step (2): per-(worker, packet) Bernoulli arrival indicators and
-    the renormalised aggregate  g_hat = sum_i s_i g_i / sum_i s_i;
+    the rescaled aggregate  g_hat = sum_i s_i g_i / sum_i s_i;
   * Section 3 "Unbiased Gradient Aggregation": the same estimator, with a
     fallback when nothing arrives;
   * Section 3 step (3): the owner's local update (plus momentum and Adam);

@@ -46,8 +46,9 @@ def store(values64, dtype: str) -> np.ndarray:
 def aggregate(g: np.ndarray, S: np.ndarray, lam: float, theta: np.ndarray):
     """Unbiased aggregate of Section 3 step (2), restated in "Unbiased Gradient
     Aggregation": per element, the sum of the contributions that arrived
-    divided by how many arrived.  When none arrived the paper only says to
-    fall back to a small regulariser; the reading here is lam * theta.
+    divided by how many arrived.  For a packet with no arrival the paper
+    leaves the substitute value open (some small regularising term); the
+    reading here is lam * theta.
 
     g: [n][E] float64, S: [n][E] in {0,1}, theta: [E] float64.
     Returns (g_hat [E], K [E], mean |contribution| [E]).
