@@ -132,11 +132,19 @@ def cpu_baseline(w, dev, packets_sample: int):
     th = dev.theta.index_select(0, ix).cpu().numpy()
     m = None if dev.m is None else dev.m.index_select(0, ix).cpu().numpy()
     v = None if dev.v is None else dev.v.index_select(0, ix).cpu().numpy()
-    p = w.loss["p"]
     t0 = time.perf_counter()
     c0 = time.process_time()
-    mg = oloss.bernoulli_arrivals(w.seed, 0, oloss.GRAD, w.n, sample, p)
-    mb = oloss.bernoulli_arrivals(w.seed, 0, oloss.BCAST, w.n, sample, p)
+    if w.loss["kind"] == "bernoulli":
+        p = w.loss["p"]
+        mg = oloss.bernoulli_arrivals(w.seed, 0, oloss.GRAD, w.n, sample, p)
+        mb = oloss.bernoulli_arrivals(w.seed, 0, oloss.BCAST, w.n, sample, p)
+    else:  # the chain runs over every packet; only the sample's columns are used
+        l = w.loss
+        zero = np.zeros(w.n, np.uint8)
+        mg = oloss.ge_arrivals(w.seed, 0, oloss.GRAD, w.n, P, l["p_gb"], l["p_bg"],
+                               l["loss_good"], l["loss_bad"], zero)[0][:, sample]
+        mb = oloss.ge_arrivals(w.seed, 0, oloss.BCAST, w.n, P, l["p_gb"], l["p_bg"],
+                               l["loss_good"], l["loss_bad"], zero)[0][:, sample]
     out = ostep.lossy_step(d=w.d, packet=w.packet, packets=sample, gdtype=w.gdtype, grads=g,
                            theta=th, m=m, v=v, replicas=reps, arrived_g=mg, arrived_b=mb,
                            opt=w.opt, t=0)
@@ -158,7 +166,9 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--workload", default=None)
+    ap.add_argument("--workload", default=None,
+                    help="one of the workloads in workloads/__init__.py (default: the N=64 "
+                         "7B-shard step)")
     ap.add_argument("--cpu-packets", type=int, default=768,
                     help="packets of the workload the CPU oracle baseline runs on")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -182,9 +192,6 @@ def main():
         sys.exit(1)
     name = args.workload or wl.METRIC_WORKLOAD
     w = wl.WORKLOADS[name]
-    if w.loss["kind"] != wl.BERNOULLI:
-        log("the benchmark times Bernoulli-loss workloads only")
-        sys.exit(1)
     copy_gbs = hbm_copy_probe()
     log(f"plain 2 GiB device copy: {copy_gbs:.0f} GB/s")
     log(f"workload {name}: n={w.n} d={w.d} packet={w.packet} P={w.num_packets}")
@@ -203,12 +210,15 @@ def main():
     lens = np.minimum((np.arange(P) + 1) * w.packet, w.d) - np.arange(P) * w.packet
     mg_dev = torch.empty((w.n, P), dtype=torch.uint8, device="cuda")
     mb_dev = torch.empty((w.n, P), dtype=torch.uint8, device="cuda")
+    ge_g = torch.zeros(w.n, dtype=torch.uint8, device="cuda")  # chain state (GE only)
+    ge_b = torch.zeros(w.n, dtype=torch.uint8, device="cuda")
     per_step_bytes = []
-    for t in range(args.warmup, args.warmup + args.steps):
-        ll.ll_masks(w.n, P, t, ll.LL_DIR_GRAD, spec, mg_dev)
-        ll.ll_masks(w.n, P, t, ll.LL_DIR_BCAST, spec, mb_dev)
-        per_step_bytes.append(algorithmic_bytes(w, mg_dev.cpu().numpy(), mb_dev.cpu().numpy(),
-                                                lens, True))
+    for t in range(args.warmup + args.steps):
+        ll.ll_masks(w.n, P, t, ll.LL_DIR_GRAD, spec, mg_dev, ge_state=ge_g)
+        ll.ll_masks(w.n, P, t, ll.LL_DIR_BCAST, spec, mb_dev, ge_state=ge_b)
+        if t >= args.warmup:
+            per_step_bytes.append(algorithmic_bytes(w, mg_dev.cpu().numpy(),
+                                                    mb_dev.cpu().numpy(), lens, True))
 
     for t in range(args.warmup):
         dev.fused(t, masks_out=False)

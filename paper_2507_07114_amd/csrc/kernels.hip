@@ -229,7 +229,22 @@ __global__ __launch_bounds__(kFinalThreads) void k_drift_final(const DriftPartia
     __shared__ unsigned long long s_stale[kFinalThreads], s_empty[kFinalThreads];
     double pair = 0.0, a = 0.0, rg = 0.0;
     unsigned long long st = 0, em = 0;
-    for (int64_t j = threadIdx.x; j < count; j += kFinalThreads) {
+    // Eight independent loads in flight per thread, then a fixed-order fold.
+    int64_t j = threadIdx.x;
+    for (; j + 7 * kFinalThreads < count; j += 8 * kFinalThreads) {
+        DriftPartial q[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) q[u] = parts[j + u * kFinalThreads];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) {
+            pair += q[u].pair;
+            a += q[u].abs_sum;
+            rg = q[u].range > rg ? q[u].range : rg;
+            st += q[u].stale;
+            em += q[u].empty;
+        }
+    }
+    for (; j < count; j += kFinalThreads) {
         const DriftPartial q = parts[j];
         pair += q.pair;
         a += q.abs_sum;
