@@ -212,10 +212,12 @@ def main():
     mb_dev = torch.empty((w.n, P), dtype=torch.uint8, device="cuda")
     ge_g = torch.zeros(w.n, dtype=torch.uint8, device="cuda")  # chain state (GE only)
     ge_b = torch.zeros(w.n, dtype=torch.uint8, device="cuda")
+    ge_ws = torch.zeros(max(ll.ll_masks_workspace_bytes(w.n, P), 256), dtype=torch.uint8,
+                        device="cuda")
     per_step_bytes = []
     for t in range(args.warmup + args.steps):
-        ll.ll_masks(w.n, P, t, ll.LL_DIR_GRAD, spec, mg_dev, ge_state=ge_g)
-        ll.ll_masks(w.n, P, t, ll.LL_DIR_BCAST, spec, mb_dev, ge_state=ge_b)
+        ll.ll_masks(w.n, P, t, ll.LL_DIR_GRAD, spec, mg_dev, ge_state=ge_g, workspace=ge_ws)
+        ll.ll_masks(w.n, P, t, ll.LL_DIR_BCAST, spec, mb_dev, ge_state=ge_b, workspace=ge_ws)
         if t >= args.warmup:
             per_step_bytes.append(algorithmic_bytes(w, mg_dev.cpu().numpy(),
                                                     mb_dev.cpu().numpy(), lens, True))

@@ -131,10 +131,17 @@ typedef struct {
  *                    chain state (0 Good, 1 Bad) at the end of the previous
  *                    step; updated to the end of this step.  Ignored (may be
  *                    NULL) for Bernoulli.
+ *   workspace        Gilbert-Elliott only: device scratch of ws_bytes >=
+ *                    ll_masks_workspace_bytes(n, num_packets); ignored (may be
+ *                    NULL) for Bernoulli.
  */
 LL_API int ll_masks(int32_t n, int64_t num_packets, uint64_t step, int32_t dir,
-             const ll_loss* loss, uint8_t* ge_state, uint8_t* arrived,
-             void* stream);
+                    const ll_loss* loss, uint8_t* ge_state, uint8_t* arrived,
+                    void* workspace, size_t ws_bytes, void* stream);
+
+/* Scratch bytes ll_masks needs for a Gilbert-Elliott process (0 on invalid
+ * sizes).  Bernoulli masks need none. */
+LL_API size_t ll_masks_workspace_bytes(int32_t n, int64_t num_packets);
 
 /*
  * Unbiased aggregate (Section 3 step (2); "Unbiased Gradient Aggregation"):
@@ -197,7 +204,8 @@ LL_API int drift_stats(int32_t n, int64_t d, int64_t packet, int32_t rdtype,
  *                           Gilbert-Elliott processes, else may be NULL.
  *   arrived_g, arrived_b    uint8 [n][P] (out, may be NULL): the masks drawn.
  *   counts                  int32 [P] (out, may be NULL): gradient arrivals.
- *   workspace, ws_bytes     scratch, ws_bytes >= ll_workspace_bytes(n, d, packet).
+ *   workspace, ws_bytes     scratch, ws_bytes >= ll_workspace_bytes(n, d, packet);
+ *                           required with drift or a Gilbert-Elliott process.
  *   drift                   ll_drift (device, out) or NULL to skip drift.
  * Lost gradient packets are never read; lost broadcast packets are read only
  * for drift and never written.
@@ -213,7 +221,8 @@ LL_API int lossy_step_fused(int32_t n, int64_t d, int64_t packet, uint64_t step,
                      void* stream);
 
 /* Bytes of device workspace that drift_stats and lossy_step_fused need for
- * these sizes (0 on invalid sizes). */
+ * these sizes (0 on invalid sizes): drift partials, two mask areas and the
+ * Gilbert-Elliott scan scratch of both directions. */
 LL_API size_t ll_workspace_bytes(int32_t n, int64_t d, int64_t packet);
 
 /* Message describing the last error on this thread ("" if none). */

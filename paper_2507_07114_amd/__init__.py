@@ -19,7 +19,8 @@ import torch
 __all__ = [
     "LossSpec", "OptSpec", "bernoulli", "gilbert_elliott", "sgd", "sgd_momentum", "adam",
     "ll_masks", "lossy_aggregate", "shard_step", "lossy_broadcast", "drift_stats",
-    "lossy_step_fused", "ll_workspace_bytes", "ll_last_error", "drift_buffer",
+    "lossy_step_fused", "ll_workspace_bytes", "ll_masks_workspace_bytes", "ll_last_error",
+    "drift_buffer",
     "read_drift", "library_path", "LossyError",
     "LL_F32", "LL_BF16", "LL_DIR_GRAD", "LL_DIR_BCAST",
 ]
@@ -81,7 +82,9 @@ _lib = None
 _vp = ctypes.c_void_p
 _i32, _i64, _u64, _f32 = ctypes.c_int32, ctypes.c_int64, ctypes.c_uint64, ctypes.c_float
 _SIGNATURES = {
-    "ll_masks": (ctypes.c_int, [_i32, _i64, _u64, _i32, ctypes.POINTER(LossSpec), _vp, _vp, _vp]),
+    "ll_masks": (ctypes.c_int, [_i32, _i64, _u64, _i32, ctypes.POINTER(LossSpec), _vp, _vp, _vp,
+                                ctypes.c_size_t, _vp]),
+    "ll_masks_workspace_bytes": (ctypes.c_size_t, [_i32, _i64]),
     "lossy_aggregate": (ctypes.c_int, [_i32, _i64, _i64, _i32, _vp, _i64, _vp, _f32, _vp, _vp,
                                        _vp, _vp]),
     "shard_step": (ctypes.c_int, [ctypes.POINTER(OptSpec), _i64, _u64, _vp, _vp, _vp, _vp, _vp]),
@@ -164,11 +167,17 @@ def _flat(t: Optional[torch.Tensor], name: str, dtype) -> Optional[int]:
 
 
 def ll_masks(n: int, num_packets: int, step: int, direction: int, loss: LossSpec,
-             arrived: torch.Tensor, ge_state: Optional[torch.Tensor] = None) -> None:
+             arrived: torch.Tensor, ge_state: Optional[torch.Tensor] = None,
+             workspace: Optional[torch.Tensor] = None) -> None:
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     _check("ll_masks", _load().ll_masks(
         n, num_packets, step, direction, ctypes.byref(loss),
         _flat(ge_state, "ge_state", torch.uint8), _flat(arrived, "arrived", torch.uint8),
-        _stream()))
+        _dev(workspace, "workspace"), ws_bytes, _stream()))
+
+
+def ll_masks_workspace_bytes(n: int, num_packets: int) -> int:
+    return int(_load().ll_masks_workspace_bytes(n, num_packets))
 
 
 def lossy_aggregate(grads: torch.Tensor, arrived: torch.Tensor, *, d: int, packet: int,

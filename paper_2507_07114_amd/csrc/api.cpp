@@ -138,17 +138,50 @@ GeParams make_ge(const ll_loss* l) {
 
 size_t round256(size_t x) { return (x + 255) & ~(size_t)255; }
 
-// Workspace layout: [drift partials][gradient masks][broadcast masks].
+// Workspace layout: [drift partials][gradient masks][broadcast masks]
+// [Gilbert-Elliott scratch for two directions], each region 256-byte aligned.
+struct GeScratch {
+    int64_t S = 0;  // segments per chain
+    size_t tmaps = 0, comps = 0, state = 0, per_dir = 0;
+};
+
+GeScratch ge_scratch(int32_t n, int64_t P) {
+    GeScratch g;
+    g.S = (P + kGeSeg - 1) / kGeSeg;
+    g.tmaps = round256((size_t)n * (size_t)g.S * kThreads);
+    g.comps = round256((size_t)n * (size_t)g.S);
+    g.state = round256((size_t)n);
+    g.per_dir = g.tmaps + g.comps + g.state;
+    return g;
+}
+
 struct WsLayout {
-    size_t partials = 0, masks = 0, total = 0;
+    size_t partials = 0, masks = 0, ge = 0, total = 0;
+    GeScratch gs;
 };
 
 WsLayout ws_layout(int32_t n, const Geometry& g) {
     WsLayout w;
     w.partials = round256((size_t)g.blocks * sizeof(DriftPartial));
     w.masks = round256((size_t)n * (size_t)g.P);
-    w.total = w.partials + 2 * w.masks;
+    w.gs = ge_scratch(n, g.P);
+    w.ge = 2 * w.gs.per_dir;
+    w.total = w.partials + 2 * w.masks + w.ge;
     return w;
+}
+
+// Fill one direction's Gilbert-Elliott job with its scratch carved from `base`.
+GeJob make_ge_job(const ll_loss* l, int dir, uint8_t* state, uint8_t* arrived,
+                  const GeScratch& gs, uint8_t* base) {
+    GeJob j;
+    j.ge = make_ge(l);
+    j.dir = (uint64_t)dir;
+    j.state = state;
+    j.arrived = arrived;
+    j.tmaps = base;
+    j.comps = base + gs.tmaps;
+    j.state_in = base + gs.tmaps + gs.comps;
+    return j;
 }
 
 }  // namespace
@@ -163,24 +196,40 @@ size_t ll_workspace_bytes(int32_t n, int64_t d, int64_t packet) {
     return ws_layout(n, g).total;
 }
 
+size_t ll_masks_workspace_bytes(int32_t n, int64_t num_packets) {
+    if (n < 1 || n > kMaxWorkers || num_packets < 0) return 0;
+    return ge_scratch(n, num_packets).per_dir;
+}
+
 int ll_masks(int32_t n, int64_t num_packets, uint64_t step, int32_t dir, const ll_loss* loss,
-             uint8_t* ge_state, uint8_t* arrived, void* stream) {
+             uint8_t* ge_state, uint8_t* arrived, void* workspace, size_t ws_bytes,
+             void* stream) {
     if (n < 1 || n > kMaxWorkers) return fail(LL_EINVAL, "n=%d outside [1, %d]", n, kMaxWorkers);
     if (num_packets < 0) return fail(LL_EINVAL, "num_packets is negative");
     if (dir != LL_DIR_GRAD && dir != LL_DIR_BCAST) return fail(LL_EINVAL, "unknown direction %d", dir);
     int r = check_loss("loss", loss);
     if (r) return r;
     if (!arrived) return fail(LL_EINVAL, "arrived is NULL");
-    if (loss->kind == LL_LOSS_GILBERT_ELLIOTT && !ge_state)
-        return fail(LL_EINVAL, "ge_state is NULL for a Gilbert-Elliott process");
+    const bool ge = loss->kind == LL_LOSS_GILBERT_ELLIOTT;
+    if (ge && !ge_state) return fail(LL_EINVAL, "ge_state is NULL for a Gilbert-Elliott process");
+    const GeScratch gs = ge_scratch(n, num_packets);
+    if (ge && (!workspace || ws_bytes < gs.per_dir))
+        return fail(LL_EINVAL, "workspace of %zu bytes is smaller than %zu", ws_bytes, gs.per_dir);
     if (num_packets == 0) return ok();
+    if ((int64_t)n * gs.S > 0x7FFFFFFFll) return fail(LL_EINVAL, "too many workgroups");
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-    if (loss->kind == LL_LOSS_BERNOULLI)
+    if (!ge)
         return hip_check(launch_masks_bernoulli(n, num_packets, step, dir, loss->seed,
                                                 threshold(loss->p), arrived, s),
                          "ll_masks");
-    return hip_check(launch_masks_ge(n, num_packets, step, dir, make_ge(loss), ge_state, arrived, s),
-                     "ll_masks");
+    GeLaunch L;
+    L.n = n;
+    L.P = num_packets;
+    L.S = gs.S;
+    L.step = step;
+    L.job[0] = make_ge_job(loss, dir, ge_state, arrived, gs, reinterpret_cast<uint8_t*>(workspace));
+    L.job[1] = L.job[0];
+    return hip_check(launch_masks_ge(L, 1, s), "ll_masks");
 }
 
 int lossy_aggregate(int32_t n, int64_t d, int64_t packet, int32_t gdtype, const void* grads,
@@ -313,7 +362,7 @@ int lossy_step_fused(int32_t n, int64_t d, int64_t packet, uint64_t step, const 
     OptParams o;
     if ((r = make_opt(opt, step, m, v, &o))) return r;
     const WsLayout w = ws_layout(n, g);
-    const bool need_ws = drift || (ge_g && !arrived_g) || (ge_b && !arrived_b);
+    const bool need_ws = drift || ge_g || ge_b;
     if (need_ws) {
         if (!workspace || ws_bytes < w.total)
             return fail(LL_EINVAL, "workspace of %zu bytes is smaller than %zu", ws_bytes, w.total);
@@ -345,20 +394,31 @@ int lossy_step_fused(int32_t n, int64_t d, int64_t packet, uint64_t step, const 
     const ll_loss* losses[2] = {loss_g, loss_b};
     uint8_t* states[2] = {ge_state_g, ge_state_b};
     uint8_t* outs[2] = {arrived_g, arrived_b};
+    GeLaunch L;
+    L.n = n;
+    L.P = g.P;
+    L.S = w.gs.S;
+    L.step = step;
+    int nge = 0;
     for (int dir = 0; dir < 2; ++dir) {
         const ll_loss* l = losses[dir];
         if (l->kind == LL_LOSS_BERNOULLI) {
             p.src[dir] = MaskSource{true, l->seed, threshold(l->p), nullptr};
         } else {
-            // Sequential chain: a scan kernel writes the masks, the step reads them.
+            // Sequential chain: the scan writes the masks, the step reads them.
             uint8_t* dst = outs[dir] ? outs[dir] : ws + w.partials + dir * w.masks;
-            r = hip_check(launch_masks_ge(n, g.P, step, dir, make_ge(l), states[dir], dst, s),
-                          "lossy_step_fused (Gilbert-Elliott masks)");
-            if (r) return r;
+            L.job[nge++] = make_ge_job(l, dir, states[dir], dst, w.gs,
+                                       ws + w.partials + 2 * w.masks + dir * w.gs.per_dir);
             p.src[dir] = MaskSource{false, 0, 0, dst};
             if (dir == 0) p.out_g = nullptr;  // already written by the scan
             else p.out_b = nullptr;
         }
+    }
+    if (nge) {
+        if ((int64_t)nge * n * w.gs.S > 0x7FFFFFFFll) return fail(LL_EINVAL, "too many workgroups");
+        if (nge == 1) L.job[1] = L.job[0];
+        r = hip_check(launch_masks_ge(L, nge, s), "lossy_step_fused (Gilbert-Elliott masks)");
+        if (r) return r;
     }
     return hip_check(launch_fused(gdtype, rdtype, p, g.blocks, reinterpret_cast<DriftOut*>(drift), s),
                      "lossy_step_fused");

@@ -19,6 +19,29 @@ struct GeParams {
     uint64_t thr_gb, thr_bg, thr_loss_good, thr_loss_bad;
 };
 
+// Gilbert-Elliott scan geometry: a thread composes kGeRun consecutive packets,
+// a workgroup one segment of kGeSeg packets.
+constexpr int kGeRun = 16;
+constexpr int64_t kGeSeg = (int64_t)kThreads * kGeRun;
+
+// One direction's Gilbert-Elliott chains (scratch regions from the workspace).
+struct GeJob {
+    GeParams ge;
+    uint64_t dir;
+    uint8_t* state;     // [n] chain state, in/out
+    uint8_t* arrived;   // [n][P] out
+    uint8_t* tmaps;     // [n][S][kThreads] per-run composite maps (scratch)
+    uint8_t* comps;     // [n][S] per-segment composite maps (scratch)
+    uint8_t* state_in;  // [n] copy of the input state (scratch)
+};
+
+struct GeLaunch {
+    int n;
+    int64_t P, S;  // packets, segments of kGeSeg packets
+    uint64_t step;
+    GeJob job[2];
+};
+
 struct AggParams {
     int n;
     int64_t d, L, P;
@@ -76,8 +99,7 @@ struct FusedParams {
 
 hipError_t launch_masks_bernoulli(int n, int64_t num_packets, uint64_t step, int dir,
                                   uint64_t seed, uint64_t thr, uint8_t* arrived, hipStream_t s);
-hipError_t launch_masks_ge(int n, int64_t num_packets, uint64_t step, int dir,
-                           const GeParams& ge, uint8_t* state, uint8_t* arrived, hipStream_t s);
+hipError_t launch_masks_ge(const GeLaunch& L, int ndir, hipStream_t s);
 hipError_t launch_aggregate(int gdtype, const AggParams& p, int64_t blocks, hipStream_t s);
 hipError_t launch_shard_step(int64_t d, const OptParams& o, float* theta, float* m, float* v,
                              const float* g_hat, hipStream_t s);

@@ -30,13 +30,20 @@ __global__ __launch_bounds__(kThreads) void k_masks_bernoulli(int n, int64_t num
     }
 }
 
-// Gilbert-Elliott masks: one workgroup per worker.  The chain's per-packet
-// transition is a map on {Good, Bad}, encoded in two bits (bit 0 = image of
-// Good, bit 1 = image of Bad).  Each thread composes the maps of a contiguous
-// run of packets, an exclusive scan of those composites across the
-// workgroup gives every run its starting state, and each thread then replays
-// its run, emitting arrivals.
-constexpr int kGeThreads = 1024;
+// Gilbert-Elliott masks.  A chain's per-packet transition is a map on
+// {Good, Bad}, encoded in two bits (bit 0 = image of Good, bit 1 = image of
+// Bad); maps compose associatively, so the chain state before any packet is
+// a prefix composition.  Two launches over (direction, worker, segment of
+// kGeSeg packets) workgroups:
+//   compose: each thread composes the maps of its run of kGeRun packets and
+//            stores the composite; a block scan gives the segment composite.
+//   apply:   each workgroup folds the composites of the earlier segments of
+//            its chain into its start state, scans its threads' composites
+//            for each run's start state, and replays its runs, emitting
+//            arrivals; the last run of the last segment stores the end state.
+// The input state is copied aside by the first launch so that the second can
+// overwrite the caller's state without racing its own readers.
+constexpr uint32_t kGeIdentity = 0x2u;  // Good -> Good, Bad -> Bad
 
 __device__ __forceinline__ uint32_t ge_apply(uint32_t map, uint32_t s) { return (map >> s) & 1u; }
 
@@ -45,46 +52,88 @@ __device__ __forceinline__ uint32_t ge_compose(uint32_t g, uint32_t f) {
     return ge_apply(g, ge_apply(f, 0)) | (ge_apply(g, ge_apply(f, 1)) << 1);
 }
 
-__global__ __launch_bounds__(kGeThreads) void k_masks_ge(int n, int64_t num_packets,
-                                                         uint64_t step, uint64_t dir,
-                                                         GeParams ge, uint8_t* state,
-                                                         uint8_t* arrived) {
-    __shared__ uint32_t s_map[kGeThreads];
-    const int i = blockIdx.x;
-    const int64_t per = (num_packets + kGeThreads - 1) / kGeThreads;
-    const int64_t k0 = (int64_t)threadIdx.x * per;
-    const int64_t k1 = k0 + per < num_packets ? k0 + per : num_packets;
+__device__ __forceinline__ uint32_t ge_packet_map(uint64_t u0, const GeParams& ge) {
+    return (u0 < ge.thr_gb ? 1u : 0u) | ((u0 < ge.thr_bg ? 0u : 1u) << 1);
+}
 
-    uint32_t f = 0x2u;  // identity: Good -> Good, Bad -> Bad
-    for (int64_t k = k0; k < k1; ++k) {
-        uint64_t w0, w1;
-        philox4x64_10((uint64_t)k, (uint64_t)i, step, dir, ge.seed, 0, w0, w1);
-        const uint64_t u0 = w0 >> 32;
-        const uint32_t mk = (u0 < ge.thr_gb ? 1u : 0u) | ((u0 < ge.thr_bg ? 0u : 1u) << 1);
-        f = ge_compose(mk, f);
+// In-place inclusive scan of kThreads maps: s[t] = f_t o ... o f_0.
+__device__ __forceinline__ void ge_block_scan(uint32_t* s) {
+    for (int off = 1; off < kThreads; off <<= 1) {
+        const uint32_t mine = s[threadIdx.x];
+        const uint32_t before = threadIdx.x >= off ? s[threadIdx.x - off] : kGeIdentity;
+        __syncthreads();
+        s[threadIdx.x] = ge_compose(mine, before);
+        __syncthreads();
     }
+}
+
+struct GeBlock {
+    int dir, i;
+    int64_t s;
+    int64_t k0, k1;  // this thread's run
+};
+
+__device__ __forceinline__ GeBlock ge_block(const GeLaunch& L) {
+    GeBlock b;
+    const int64_t per_dir = (int64_t)L.n * L.S;
+    const int64_t id = blockIdx.x;
+    b.dir = (int)(id / per_dir);
+    const int64_t rem = id - b.dir * per_dir;
+    b.i = (int)(rem / L.S);
+    b.s = rem - (int64_t)b.i * L.S;
+    b.k0 = b.s * kGeSeg + (int64_t)threadIdx.x * kGeRun;
+    b.k1 = b.k0 + kGeRun < L.P ? b.k0 + kGeRun : L.P;
+    return b;
+}
+
+__global__ __launch_bounds__(kThreads) void k_ge_compose(GeLaunch L) {
+    __shared__ uint32_t s_map[kThreads];
+    const GeBlock b = ge_block(L);
+    const GeJob& J = L.job[b.dir];
+    uint32_t f = kGeIdentity;
+    for (int64_t k = b.k0; k < b.k1; ++k) {
+        uint64_t w0, w1;
+        philox4x64_10((uint64_t)k, (uint64_t)b.i, L.step, J.dir, J.ge.seed, 0, w0, w1);
+        f = ge_compose(ge_packet_map(w0 >> 32, J.ge), f);
+    }
+    const int64_t seg = (int64_t)b.i * L.S + b.s;
+    J.tmaps[seg * kThreads + threadIdx.x] = (uint8_t)f;
     s_map[threadIdx.x] = f;
     __syncthreads();
-    // Inclusive Hillis-Steele scan: s_map[t] = f_t o ... o f_0.
-    for (int off = 1; off < kGeThreads; off <<= 1) {
-        const uint32_t mine = s_map[threadIdx.x];
-        const uint32_t before = threadIdx.x >= off ? s_map[threadIdx.x - off] : 0x2u;
+    ge_block_scan(s_map);
+    if (threadIdx.x == kThreads - 1) J.comps[seg] = (uint8_t)s_map[kThreads - 1];
+    if (b.s == 0 && threadIdx.x == 0) J.state_in[b.i] = J.state[b.i] ? 1 : 0;
+}
+
+__global__ __launch_bounds__(kThreads) void k_ge_apply(GeLaunch L) {
+    __shared__ uint32_t s_run[kThreads];
+    __shared__ uint32_t s_seg[kThreads];
+    const GeBlock b = ge_block(L);
+    const GeJob& J = L.job[b.dir];
+    const int64_t row = (int64_t)b.i * L.S;
+    // Composition of the earlier segments of this chain, 256 at a time.
+    uint32_t before = kGeIdentity;
+    for (int64_t base = 0; base < b.s; base += kThreads) {
+        const int64_t j = base + threadIdx.x;
+        s_seg[threadIdx.x] = j < b.s ? J.comps[row + j] : kGeIdentity;
         __syncthreads();
-        s_map[threadIdx.x] = ge_compose(mine, before);
+        ge_block_scan(s_seg);
+        before = ge_compose(s_seg[kThreads - 1], before);
         __syncthreads();
     }
-    const uint32_t s_in = state[i] ? 1u : 0u;
-    uint32_t s = threadIdx.x == 0 ? s_in : ge_apply(s_map[threadIdx.x - 1], s_in);
-    for (int64_t k = k0; k < k1; ++k) {
+    s_run[threadIdx.x] = J.tmaps[(row + b.s) * kThreads + threadIdx.x];
+    __syncthreads();
+    ge_block_scan(s_run);
+    const uint32_t own_prefix = threadIdx.x == 0 ? kGeIdentity : s_run[threadIdx.x - 1];
+    uint32_t x = ge_apply(own_prefix, ge_apply(before, J.state_in[b.i]));
+    for (int64_t k = b.k0; k < b.k1; ++k) {
         uint64_t w0, w1;
-        philox4x64_10((uint64_t)k, (uint64_t)i, step, dir, ge.seed, 0, w0, w1);
-        const uint64_t u0 = w0 >> 32, u1 = w1 >> 32;
-        s = s == 0 ? (u0 < ge.thr_gb ? 1u : 0u) : (u0 < ge.thr_bg ? 0u : 1u);
-        const bool lost = u1 < (s ? ge.thr_loss_bad : ge.thr_loss_good);
-        arrived[(int64_t)i * num_packets + k] = lost ? 0 : 1;
+        philox4x64_10((uint64_t)k, (uint64_t)b.i, L.step, J.dir, J.ge.seed, 0, w0, w1);
+        x = ge_apply(ge_packet_map(w0 >> 32, J.ge), x);
+        const bool lost = (w1 >> 32) < (x ? J.ge.thr_loss_bad : J.ge.thr_loss_good);
+        J.arrived[(int64_t)b.i * L.P + k] = lost ? 0 : 1;
     }
-    __syncthreads();  // every thread has read state[i]
-    if (threadIdx.x == kGeThreads - 1) state[i] = (uint8_t)ge_apply(s_map[kGeThreads - 1], s_in);
+    if (b.s == L.S - 1 && threadIdx.x == kThreads - 1) J.state[b.i] = (uint8_t)x;
 }
 
 // ---------------------------------------------------------------------------
@@ -402,11 +451,12 @@ hipError_t launch_masks_bernoulli(int n, int64_t num_packets, uint64_t step, int
     return hipGetLastError();
 }
 
-hipError_t launch_masks_ge(int n, int64_t num_packets, uint64_t step, int dir,
-                           const GeParams& ge, uint8_t* state, uint8_t* arrived,
-                           hipStream_t s) {
-    hipLaunchKernelGGL(k_masks_ge, dim3((unsigned)n), dim3(kGeThreads), 0, s, n, num_packets,
-                       step, (uint64_t)dir, ge, state, arrived);
+hipError_t launch_masks_ge(const GeLaunch& L, int ndir, hipStream_t s) {
+    const int64_t blocks = (int64_t)ndir * L.n * L.S;
+    hipLaunchKernelGGL(k_ge_compose, dim3((unsigned)blocks), dim3(kThreads), 0, s, L);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_ge_apply, dim3((unsigned)blocks), dim3(kThreads), 0, s, L);
     return hipGetLastError();
 }
 

@@ -21,7 +21,8 @@ def _declared():
 def test_header_declares_the_boundary():
     names = set(_declared())
     assert names == {"ll_masks", "lossy_aggregate", "shard_step", "lossy_broadcast",
-                     "drift_stats", "lossy_step_fused", "ll_workspace_bytes", "ll_last_error"}
+                     "drift_stats", "lossy_step_fused", "ll_workspace_bytes",
+                     "ll_masks_workspace_bytes", "ll_last_error"}
 
 
 def test_library_exports_every_declared_symbol():
@@ -44,10 +45,15 @@ def test_workspace_bytes_host_logic():
     # each rounded up to 256 B.
     def r256(x):
         return (x + 255) // 256 * 256
+    def ge(n, P):  # per direction: run maps, segment maps, state copy
+        S = (P + 4095) // 4096
+        return r256(n * S * 256) + r256(n * S) + r256(n)
     n, d, L = 64, 105_250_000, 4096
     P = (d + L - 1) // L
-    assert ll.ll_workspace_bytes(n, d, L) == r256(P * 2 * 32) + 2 * r256(n * P)
-    assert ll.ll_workspace_bytes(4, 10, 8) == 256 + 2 * 256
+    assert ll.ll_workspace_bytes(n, d, L) == r256(P * 2 * 32) + 2 * r256(n * P) + 2 * ge(n, P)
+    assert ll.ll_workspace_bytes(4, 10, 8) == 256 + 2 * 256 + 2 * ge(4, 2)
+    assert ll.ll_masks_workspace_bytes(16, 65536) == ge(16, 65536)
+    assert ll.ll_masks_workspace_bytes(0, 5) == 0
     assert ll.ll_workspace_bytes(0, 10, 8) == 0      # invalid n
     assert ll.ll_workspace_bytes(4, 10, 12) == 0     # packet not a multiple of 8
     assert ll.ll_workspace_bytes(4, -1, 8) == 0
@@ -87,15 +93,18 @@ def test_masks_and_opt_validation():
     bad_p = ll.bernoulli(1.5)
     fm = lib.ll_masks
     fm.argtypes = [ctypes.c_int32, ctypes.c_int64, ctypes.c_uint64, ctypes.c_int32,
-                   ctypes.POINTER(ll.LossSpec), ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
-    assert fm(4, 10, 0, 0, ctypes.byref(bad_p), None, 16, None) == -1
+                   ctypes.POINTER(ll.LossSpec), ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                   ctypes.c_size_t, ctypes.c_void_p]
+    assert fm(4, 10, 0, 0, ctypes.byref(bad_p), None, 16, None, 0, None) == -1
     assert "p outside" in lib.ll_last_error().decode()
     ge = ll.gilbert_elliott(0.1, 0.2, 0.0, 0.5)
-    assert fm(4, 10, 0, 0, ctypes.byref(ge), None, 16, None) == -1
+    assert fm(4, 10, 0, 0, ctypes.byref(ge), None, 16, None, 0, None) == -1
     assert "ge_state" in lib.ll_last_error().decode()
-    assert fm(4, 10, 0, 3, ctypes.byref(ll.bernoulli(0.1)), None, 16, None) == -1
+    assert fm(4, 10, 0, 0, ctypes.byref(ge), 16, 16, None, 0, None) == -1
+    assert "workspace" in lib.ll_last_error().decode()
+    assert fm(4, 10, 0, 3, ctypes.byref(ll.bernoulli(0.1)), None, 16, None, 0, None) == -1
     # Zero packets is a valid no-op that touches no device.
-    assert fm(4, 0, 0, 0, ctypes.byref(ll.bernoulli(0.1)), None, 16, None) == 0
+    assert fm(4, 0, 0, 0, ctypes.byref(ll.bernoulli(0.1)), None, 16, None, 0, None) == 0
 
     fs = lib.shard_step
     fs.argtypes = [ctypes.POINTER(ll.OptSpec), ctypes.c_int64, ctypes.c_uint64, ctypes.c_void_p,

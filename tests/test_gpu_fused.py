@@ -37,11 +37,13 @@ def _stagewise(dev: parity.DeviceState, step: int):
     spec = parity.loss_spec(w)
     P = w.num_packets
     g_hat = torch.empty(w.d, dtype=torch.float32, device=DEV)
-    ll.ll_masks(w.n, P, step, ll.LL_DIR_GRAD, spec, dev.arrived_g, ge_state=dev.ge_g)
+    ll.ll_masks(w.n, P, step, ll.LL_DIR_GRAD, spec, dev.arrived_g, ge_state=dev.ge_g,
+                workspace=dev.workspace)
     ll.lossy_aggregate(dev.grads, dev.arrived_g, d=w.d, packet=w.packet, g_hat=g_hat,
                        counts=dev.counts, theta=dev.theta)
     ll.shard_step(parity.opt_spec(w), step, dev.theta, g_hat, m=dev.m, v=dev.v)
-    ll.ll_masks(w.n, P, step, ll.LL_DIR_BCAST, spec, dev.arrived_b, ge_state=dev.ge_b)
+    ll.ll_masks(w.n, P, step, ll.LL_DIR_BCAST, spec, dev.arrived_b, ge_state=dev.ge_b,
+                workspace=dev.workspace)
     ll.lossy_broadcast(dev.theta, dev.replicas, dev.arrived_b, d=w.d, packet=w.packet)
     ll.drift_stats(dev.replicas, d=w.d, packet=w.packet, workspace=dev.workspace,
                    out=dev.drift, theta=dev.theta, arrived_bc=dev.arrived_b)

@@ -58,18 +58,21 @@ def test_bernoulli_masks_bit_exact(n, P, p):
         assert np.array_equal(out.cpu().numpy(), want)
 
 
-@pytest.mark.parametrize("n,P,steps", [(3, 5, 3), (7, 1500, 2), (16, 65536, 3), (2, 1024, 2)])
+@pytest.mark.parametrize("n,P,steps", [(3, 5, 3), (7, 1500, 2), (16, 65536, 3), (2, 1024, 2),
+                                        (5, 4096 * 3 + 17, 2),    # ragged last segment
+                                        (1, 1_100_000, 1)])       # > 256 segments per chain
 def test_gilbert_elliott_masks_and_state_bit_exact(n, P, steps):
     p_gb, p_bg, lg, lb = 0.01, 0.2, 0.0, 0.5
     if P < 2000:  # make short chains switch often
         p_gb, p_bg, lg, lb = 0.3, 0.4, 0.1, 0.6
     spec = ll.gilbert_elliott(p_gb, p_bg, lg, lb, seed=3)
     st_dev = torch.zeros(n, dtype=torch.uint8, device=DEV)
+    ws = torch.zeros(ll.ll_masks_workspace_bytes(n, P), dtype=torch.uint8, device=DEV)
     st_orc = np.zeros(n, np.uint8)
     out = torch.zeros((n, P), dtype=torch.uint8, device=DEV)
     for t in range(steps):
         print(f"GE masks n={n} P={P} step={t}", flush=True)
-        ll.ll_masks(n, P, t, 1, spec, out, ge_state=st_dev)
+        ll.ll_masks(n, P, t, 1, spec, out, ge_state=st_dev, workspace=ws)
         want, st_orc = oloss.ge_arrivals(3, t, 1, n, P, p_gb, p_bg, lg, lb, st_orc)
         assert np.array_equal(out.cpu().numpy(), want)
         assert np.array_equal(st_dev.cpu().numpy(), st_orc)
