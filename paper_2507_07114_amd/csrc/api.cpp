@@ -15,6 +15,7 @@ using namespace lossy;
 
 static_assert(sizeof(ll_drift) == sizeof(DriftOut), "ll_drift layout");
 static_assert(sizeof(DriftPartial) == 32, "partial layout");
+static_assert(sizeof(DriftAcc) == 40, "second-level partial layout");
 
 namespace {
 
@@ -155,14 +156,17 @@ GeScratch ge_scratch(int32_t n, int64_t P) {
     return g;
 }
 
+// The partials region holds one partial per workgroup followed by the
+// kReduceGroups second-level partials.
 struct WsLayout {
-    size_t partials = 0, masks = 0, ge = 0, total = 0;
+    size_t partials = 0, groups_off = 0, masks = 0, ge = 0, total = 0;
     GeScratch gs;
 };
 
 WsLayout ws_layout(int32_t n, const Geometry& g) {
     WsLayout w;
-    w.partials = round256((size_t)g.blocks * sizeof(DriftPartial));
+    w.groups_off = round256((size_t)g.blocks * sizeof(DriftPartial));
+    w.partials = w.groups_off + round256((size_t)kReduceGroups * sizeof(DriftAcc));
     w.masks = round256((size_t)n * (size_t)g.P);
     w.gs = ge_scratch(n, g.P);
     w.ge = 2 * w.gs.per_dir;
@@ -328,6 +332,7 @@ int drift_stats(int32_t n, int64_t d, int64_t packet, int32_t rdtype, const void
     p.theta = theta;
     p.arrived = arrived_bc;
     p.partials = reinterpret_cast<DriftPartial*>(workspace);
+    p.groups = reinterpret_cast<DriftAcc*>(reinterpret_cast<uint8_t*>(workspace) + w.groups_off);
     return hip_check(launch_drift(rdtype, p, g.blocks, n, d, theta != nullptr,
                                   reinterpret_cast<DriftOut*>(out), s),
                      "drift_stats");
@@ -390,6 +395,7 @@ int lossy_step_fused(int32_t n, int64_t d, int64_t packet, uint64_t step, const 
     p.replicas = replicas;
     p.ld_r = ld_r;
     p.partials = drift ? reinterpret_cast<DriftPartial*>(ws) : nullptr;
+    p.groups = drift ? reinterpret_cast<DriftAcc*>(ws + w.groups_off) : nullptr;
 
     const ll_loss* losses[2] = {loss_g, loss_b};
     uint8_t* states[2] = {ge_state_g, ge_state_b};

@@ -14,10 +14,37 @@ struct DriftOut {
     unsigned long long stale_packets, empty_packets;
 };
 
+// Running totals of drift partials (second reduction level), 64-bit counts.
+struct DriftAcc {
+    double pair, abs_sum, range;
+    unsigned long long stale, empty;
+    __device__ __forceinline__ void zero() {
+        pair = abs_sum = range = 0.0;
+        stale = empty = 0;
+    }
+    __device__ __forceinline__ void add(const DriftPartial& q) {
+        pair += q.pair;
+        abs_sum += q.abs_sum;
+        range = q.range > range ? q.range : range;
+        stale += q.stale;
+        empty += q.empty;
+    }
+    __device__ __forceinline__ void add(const DriftAcc& q) {
+        pair += q.pair;
+        abs_sum += q.abs_sum;
+        range = q.range > range ? q.range : range;
+        stale += q.stale;
+        empty += q.empty;
+    }
+};
+
 struct GeParams {
     uint64_t seed;
     uint64_t thr_gb, thr_bg, thr_loss_good, thr_loss_bad;
 };
+
+// Workgroups of the first drift reduction level.
+constexpr int kReduceGroups = 256;
 
 // Gilbert-Elliott scan geometry: a thread composes kGeRun consecutive packets,
 // a workgroup one segment of kGeSeg packets.
@@ -74,6 +101,7 @@ struct DriftParams {
     const float* theta;
     const uint8_t* arrived;
     DriftPartial* partials;
+    DriftAcc* groups;  // [kReduceGroups] second-level partials
 };
 
 struct FusedParams {
@@ -95,6 +123,7 @@ struct FusedParams {
     void* replicas;
     int64_t ld_r;
     DriftPartial* partials;
+    DriftAcc* groups;  // [kReduceGroups] second-level partials
 };
 
 hipError_t launch_masks_bernoulli(int n, int64_t num_packets, uint64_t step, int dir,

@@ -268,69 +268,72 @@ __global__ __launch_bounds__(kThreads) void k_drift(DriftParams p) {
     block_reduce_partial(pair, abs_sum, range, stale, 0, p.partials + blockIdx.x);
 }
 
-// Fixed-order reduction of the partials into the ll_drift record.
-constexpr int kFinalThreads = 1024;
-
-__global__ __launch_bounds__(kFinalThreads) void k_drift_final(const DriftPartial* parts,
-                                                               int64_t count, int n, int64_t d,
-                                                               int have_master, DriftOut* out) {
-    __shared__ double s_pair[kFinalThreads], s_abs[kFinalThreads], s_rng[kFinalThreads];
-    __shared__ unsigned long long s_stale[kFinalThreads], s_empty[kFinalThreads];
-    double pair = 0.0, a = 0.0, rg = 0.0;
-    unsigned long long st = 0, em = 0;
-    // Eight independent loads in flight per thread, then a fixed-order fold.
-    int64_t j = threadIdx.x;
-    for (; j + 7 * kFinalThreads < count; j += 8 * kFinalThreads) {
-        DriftPartial q[8];
-#pragma unroll
-        for (int u = 0; u < 8; ++u) q[u] = parts[j + u * kFinalThreads];
-#pragma unroll
-        for (int u = 0; u < 8; ++u) {
-            pair += q[u].pair;
-            a += q[u].abs_sum;
-            rg = q[u].range > rg ? q[u].range : rg;
-            st += q[u].stale;
-            em += q[u].empty;
-        }
-    }
-    for (; j < count; j += kFinalThreads) {
-        const DriftPartial q = parts[j];
-        pair += q.pair;
-        a += q.abs_sum;
-        rg = q.range > rg ? q.range : rg;
-        st += q.stale;
-        em += q.empty;
-    }
-    s_pair[threadIdx.x] = pair;
-    s_abs[threadIdx.x] = a;
-    s_rng[threadIdx.x] = rg;
-    s_stale[threadIdx.x] = st;
-    s_empty[threadIdx.x] = em;
+// Fixed-order reduction of the per-workgroup partials into the ll_drift
+// record, in two launches: kReduceGroups workgroups each fold a contiguous
+// range of partials, then one workgroup folds those and writes the record.
+// Fixed-order tree over the workgroup; thread 0 returns the total.
+__device__ __forceinline__ DriftAcc block_fold(DriftAcc a) {
+    __shared__ DriftAcc s_acc[kThreads];
+    s_acc[threadIdx.x] = a;
     __syncthreads();
-    for (int off = kFinalThreads / 2; off > 0; off >>= 1) {
-        if (threadIdx.x < off) {
-            s_pair[threadIdx.x] += s_pair[threadIdx.x + off];
-            s_abs[threadIdx.x] += s_abs[threadIdx.x + off];
-            const double o = s_rng[threadIdx.x + off];
-            s_rng[threadIdx.x] = o > s_rng[threadIdx.x] ? o : s_rng[threadIdx.x];
-            s_stale[threadIdx.x] += s_stale[threadIdx.x + off];
-            s_empty[threadIdx.x] += s_empty[threadIdx.x + off];
-        }
+    for (int off = kThreads / 2; off > 0; off >>= 1) {
+        if (threadIdx.x < off) s_acc[threadIdx.x].add(s_acc[threadIdx.x + off]);
         __syncthreads();
     }
+    return s_acc[0];
+}
+
+__global__ __launch_bounds__(kThreads) void k_drift_reduce(const DriftPartial* parts, int64_t count,
+                                                           DriftAcc* out) {
+    const int64_t per = (count + kReduceGroups - 1) / kReduceGroups;
+    const int64_t lo = (int64_t)blockIdx.x * per;
+    const int64_t hi = lo + per < count ? lo + per : count;
+    DriftAcc a;
+    a.zero();
+    int64_t j = lo + threadIdx.x;
+    for (; j + 3 * kThreads < hi; j += 4 * kThreads) {
+        DriftPartial q[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) q[u] = parts[j + u * kThreads];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) a.add(q[u]);
+    }
+    for (; j < hi; j += kThreads) a.add(parts[j]);
+    const DriftAcc t = block_fold(a);
+    if (threadIdx.x == 0) out[blockIdx.x] = t;
+}
+
+__global__ __launch_bounds__(kThreads) void k_drift_final(const DriftAcc* groups, int n,
+                                                          int64_t d, int have_master,
+                                                          DriftOut* out) {
+    DriftAcc a;
+    a.zero();
+    for (int j = threadIdx.x; j < kReduceGroups; j += kThreads) a.add(groups[j]);
+    const DriftAcc t = block_fold(a);
     if (threadIdx.x == 0) {
         const double pairs = (double)n * (double)(n - 1) * 0.5;
         const double denom = (double)d * pairs;
         DriftOut r;
-        r.max_abs = s_rng[0];
-        r.mean_sq = denom > 0.0 ? s_pair[0] / denom : 0.0;
+        r.max_abs = t.range;
+        r.mean_sq = denom > 0.0 ? t.pair / denom : 0.0;
         r.rms = sqrt(r.mean_sq);
         r.mean_abs_to_master =
-            have_master ? (d > 0 ? s_abs[0] / ((double)n * (double)d) : 0.0) : (double)NAN;
-        r.stale_packets = s_stale[0];
-        r.empty_packets = s_empty[0];
+            have_master ? (d > 0 ? t.abs_sum / ((double)n * (double)d) : 0.0) : (double)NAN;
+        r.stale_packets = t.stale;
+        r.empty_packets = t.empty;
         *out = r;
     }
+}
+
+static hipError_t launch_drift_reduce(const DriftPartial* parts, int64_t count, DriftAcc* groups,
+                                      int n, int64_t d, int have_master, DriftOut* out,
+                                      hipStream_t s) {
+    hipLaunchKernelGGL(k_drift_reduce, dim3(kReduceGroups), dim3(kThreads), 0, s, parts, count,
+                       groups);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(k_drift_final, dim3(1), dim3(kThreads), 0, s, groups, n, d, have_master, out);
+    return hipGetLastError();
 }
 
 // ---------------------------------------------------------------------------
@@ -492,9 +495,7 @@ hipError_t launch_drift(int rdtype, const DriftParams& p, int64_t blocks, int n,
         hipLaunchKernelGGL(k_drift<F32>, dim3((unsigned)blocks), dim3(kThreads), 0, s, p);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k_drift_final, dim3(1), dim3(kFinalThreads), 0, s, p.partials, blocks, n,
-                       d, have_master, out);
-    return hipGetLastError();
+    return launch_drift_reduce(p.partials, blocks, p.groups, n, d, have_master, out, s);
 }
 
 template <class G, class R>
@@ -516,9 +517,7 @@ hipError_t launch_fused(int gdtype, int rdtype, const FusedParams& p, int64_t bl
     else launch_fused_gr<F32, F32>(dr, p, blocks, s);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || !dr) return e;
-    hipLaunchKernelGGL(k_drift_final, dim3(1), dim3(kFinalThreads), 0, s, p.partials, blocks,
-                       p.n, p.d, 1, drift);
-    return hipGetLastError();
+    return launch_drift_reduce(p.partials, blocks, p.groups, p.n, p.d, 1, drift, s);
 }
 
 hipError_t launch_drift_zero(DriftOut* out, hipStream_t s) {

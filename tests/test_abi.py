@@ -41,8 +41,9 @@ def test_struct_layouts():
 
 
 def test_workspace_bytes_host_logic():
-    # partials: 32 B per workgroup (P * ceil(L / 2048)), then two n*P mask areas,
-    # each rounded up to 256 B.
+    # partials: 32 B per workgroup (P * ceil(L / 2048)) and 256 second-level
+    # ones of 40 B, then two n*P mask areas and the Gilbert-Elliott scan scratch of
+    # both directions, each region rounded up to 256 B.
     def r256(x):
         return (x + 255) // 256 * 256
     def ge(n, P):  # per direction: run maps, segment maps, state copy
@@ -50,8 +51,10 @@ def test_workspace_bytes_host_logic():
         return r256(n * S * 256) + r256(n * S) + r256(n)
     n, d, L = 64, 105_250_000, 4096
     P = (d + L - 1) // L
-    assert ll.ll_workspace_bytes(n, d, L) == r256(P * 2 * 32) + 2 * r256(n * P) + 2 * ge(n, P)
-    assert ll.ll_workspace_bytes(4, 10, 8) == 256 + 2 * 256 + 2 * ge(4, 2)
+    groups = 256 * 40  # second-level drift partials
+    assert ll.ll_workspace_bytes(n, d, L) == (r256(P * 2 * 32) + groups + 2 * r256(n * P)
+                                              + 2 * ge(n, P))
+    assert ll.ll_workspace_bytes(4, 10, 8) == 256 + groups + 2 * 256 + 2 * ge(4, 2)
     assert ll.ll_masks_workspace_bytes(16, 65536) == ge(16, 65536)
     assert ll.ll_masks_workspace_bytes(0, 5) == 0
     assert ll.ll_workspace_bytes(0, 10, 8) == 0      # invalid n
