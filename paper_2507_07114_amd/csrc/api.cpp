@@ -48,9 +48,11 @@ uint64_t threshold(double p) { return (uint64_t)std::ceil(p * 4294967296.0); }
 
 bool prob_ok(double p) { return p >= 0.0 && p <= 1.0; }
 
+// Packets and the largest per-packet grid any element type can need (the
+// smallest workgroup, kMinPacketThreads, gives the most chunks per packet);
+// drift partials and grid limits are sized for that worst case.
 struct Geometry {
-    int64_t P = 0;    // packets
-    int cpp = 0;      // workgroup chunks per packet
+    int64_t P = 0;
     int64_t blocks = 0;
 };
 
@@ -61,8 +63,8 @@ int check_shape(int32_t n, int64_t d, int64_t packet, Geometry* g) {
     if (packet < 8 || packet % 8 != 0)
         return fail(LL_EINVAL, "packet=%lld must be a positive multiple of 8", (long long)packet);
     g->P = (d + packet - 1) / packet;
-    g->cpp = (int)((packet + kChunk - 1) / kChunk);
-    g->blocks = g->P * g->cpp;
+    const int64_t chunk = (int64_t)kMinPacketThreads * kElems;
+    g->blocks = g->P * ((packet + chunk - 1) / chunk);
     if (g->blocks > 0x7FFFFFFFll)
         return fail(LL_EINVAL, "too many workgroups (%lld)", (long long)g->blocks);
     return LL_OK;
@@ -253,7 +255,7 @@ int lossy_aggregate(int32_t n, int64_t d, int64_t packet, int32_t gdtype, const 
     p.d = d;
     p.L = packet;
     p.P = g.P;
-    p.cpp = g.cpp;
+    p.cpp = 0;
     p.grads = grads;
     p.ld = ld_g;
     p.arrived = arrived;
@@ -261,7 +263,7 @@ int lossy_aggregate(int32_t n, int64_t d, int64_t packet, int32_t gdtype, const 
     p.theta = theta;
     p.g_hat = g_hat;
     p.counts = counts;
-    return hip_check(launch_aggregate(gdtype, p, g.blocks, reinterpret_cast<hipStream_t>(stream)),
+    return hip_check(launch_aggregate(gdtype, p, reinterpret_cast<hipStream_t>(stream)),
                      "lossy_aggregate");
 }
 
@@ -274,7 +276,8 @@ int shard_step(const ll_opt* opt, int64_t d, uint64_t step, float* theta, float*
     if (r) return r;
     if ((r = check_vec("theta", theta, true))) return r;
     if ((r = check_vec("g_hat", g_hat, true))) return r;
-    if ((d + kChunk - 1) / kChunk > 0x7FFFFFFFll) return fail(LL_EINVAL, "d too large");
+    if ((d + kThreads * kElems - 1) / (kThreads * kElems) > 0x7FFFFFFFll)
+        return fail(LL_EINVAL, "d too large");
     return hip_check(launch_shard_step(d, o, theta, m, v, g_hat,
                                        reinterpret_cast<hipStream_t>(stream)),
                      "shard_step");
@@ -295,12 +298,12 @@ int lossy_broadcast(int32_t n, int64_t d, int64_t packet, const float* theta, in
     p.d = d;
     p.L = packet;
     p.P = g.P;
-    p.cpp = g.cpp;
+    p.cpp = 0;
     p.theta = theta;
     p.replicas = replicas;
     p.ld = ld_r;
     p.arrived = arrived_bc;
-    return hip_check(launch_broadcast(rdtype, p, g.blocks, reinterpret_cast<hipStream_t>(stream)),
+    return hip_check(launch_broadcast(rdtype, p, reinterpret_cast<hipStream_t>(stream)),
                      "lossy_broadcast");
 }
 
@@ -326,14 +329,14 @@ int drift_stats(int32_t n, int64_t d, int64_t packet, int32_t rdtype, const void
     p.d = d;
     p.L = packet;
     p.P = g.P;
-    p.cpp = g.cpp;
+    p.cpp = 0;
     p.replicas = replicas;
     p.ld = ld_r;
     p.theta = theta;
     p.arrived = arrived_bc;
     p.partials = reinterpret_cast<DriftPartial*>(workspace);
     p.groups = reinterpret_cast<DriftAcc*>(reinterpret_cast<uint8_t*>(workspace) + w.groups_off);
-    return hip_check(launch_drift(rdtype, p, g.blocks, n, d, theta != nullptr,
+    return hip_check(launch_drift(rdtype, p, n, d, theta != nullptr,
                                   reinterpret_cast<DriftOut*>(out), s),
                      "drift_stats");
 }
@@ -380,7 +383,7 @@ int lossy_step_fused(int32_t n, int64_t d, int64_t packet, uint64_t step, const 
     p.d = d;
     p.L = packet;
     p.P = g.P;
-    p.cpp = g.cpp;
+    p.cpp = 0;
     p.step = step;
     p.out_g = arrived_g;
     p.out_b = arrived_b;
@@ -426,7 +429,7 @@ int lossy_step_fused(int32_t n, int64_t d, int64_t packet, uint64_t step, const 
         r = hip_check(launch_masks_ge(L, nge, s), "lossy_step_fused (Gilbert-Elliott masks)");
         if (r) return r;
     }
-    return hip_check(launch_fused(gdtype, rdtype, p, g.blocks, reinterpret_cast<DriftOut*>(drift), s),
+    return hip_check(launch_fused(gdtype, rdtype, p, reinterpret_cast<DriftOut*>(drift), s),
                      "lossy_step_fused");
 }
 

@@ -72,7 +72,7 @@ struct GeLaunch {
 struct AggParams {
     int n;
     int64_t d, L, P;
-    int cpp;  // chunks per packet
+    int cpp;  // chunks per packet (set by the launcher)
     const void* grads;
     int64_t ld;
     const uint8_t* arrived;
@@ -129,14 +129,14 @@ struct FusedParams {
 hipError_t launch_masks_bernoulli(int n, int64_t num_packets, uint64_t step, int dir,
                                   uint64_t seed, uint64_t thr, uint8_t* arrived, hipStream_t s);
 hipError_t launch_masks_ge(const GeLaunch& L, int ndir, hipStream_t s);
-hipError_t launch_aggregate(int gdtype, const AggParams& p, int64_t blocks, hipStream_t s);
+hipError_t launch_aggregate(int gdtype, const AggParams& p, hipStream_t s);
 hipError_t launch_shard_step(int64_t d, const OptParams& o, float* theta, float* m, float* v,
                              const float* g_hat, hipStream_t s);
-hipError_t launch_broadcast(int rdtype, const BcastParams& p, int64_t blocks, hipStream_t s);
-hipError_t launch_drift(int rdtype, const DriftParams& p, int64_t blocks, int n, int64_t d,
-                        int have_master, DriftOut* out, hipStream_t s);
-hipError_t launch_fused(int gdtype, int rdtype, const FusedParams& p, int64_t blocks,
-                        DriftOut* drift, hipStream_t s);
+hipError_t launch_broadcast(int rdtype, const BcastParams& p, hipStream_t s);
+hipError_t launch_drift(int rdtype, const DriftParams& p, int n, int64_t d, int have_master,
+                        DriftOut* out, hipStream_t s);
+hipError_t launch_fused(int gdtype, int rdtype, const FusedParams& p, DriftOut* drift,
+                        hipStream_t s);
 hipError_t launch_drift_zero(DriftOut* out, hipStream_t s);
 
 }  // namespace lossy

@@ -146,6 +146,7 @@ struct Chunk {
     int nv;       // valid elements of this thread (0..8)
 };
 
+template <int NT>
 __device__ __forceinline__ Chunk chunk_of(int64_t d, int64_t L, int cpp) {
     Chunk ch;
     const int64_t b = blockIdx.x;
@@ -153,7 +154,7 @@ __device__ __forceinline__ Chunk chunk_of(int64_t d, int64_t L, int cpp) {
     ch.c = (int)(b - ch.k * cpp);
     const int64_t pk0 = ch.k * L;
     const int64_t pend = pk0 + L < d ? pk0 + L : d;
-    ch.e0 = pk0 + (int64_t)ch.c * kChunk + (int64_t)threadIdx.x * kElems;
+    ch.e0 = pk0 + (int64_t)ch.c * (NT * kElems) + (int64_t)threadIdx.x * kElems;
     const int64_t rem = pend - ch.e0;
     ch.nv = rem <= 0 ? 0 : (rem >= 8 ? 8 : (int)rem);
     return ch;
@@ -163,12 +164,13 @@ __device__ __forceinline__ Chunk chunk_of(int64_t d, int64_t L, int cpp) {
 // One-stage entry points
 // ---------------------------------------------------------------------------
 template <class G>
-__global__ __launch_bounds__(kThreads) void k_aggregate(AggParams p) {
+__global__ __launch_bounds__(G::kPacketThreads) void k_aggregate(AggParams p) {
+    constexpr int NT = G::kPacketThreads;
     __shared__ uint64_t s_words[1][kMaxWords];
-    const Chunk ch = chunk_of(p.d, p.L, p.cpp);
+    const Chunk ch = chunk_of<NT>(p.d, p.L, p.cpp);
     MaskSource src{false, 0, 0, p.arrived};
     const int dirs[1] = {0};
-    stage_masks(1, &src, p.n, p.P, ch.k, 0, dirs, s_words);
+    stage_masks<NT>(1, &src, p.n, p.P, ch.k, 0, dirs, s_words);
     const int nw = (p.n + 63) >> 6;
     const int K = popcount_words(s_words[0], nw);
     if (ch.c == 0 && threadIdx.x == 0 && p.counts) p.counts[ch.k] = K;
@@ -199,12 +201,13 @@ __global__ __launch_bounds__(kThreads) void k_shard_step(int64_t d, OptParams o,
 }
 
 template <class R>
-__global__ __launch_bounds__(kThreads) void k_broadcast(BcastParams p) {
+__global__ __launch_bounds__(R::kPacketThreads) void k_broadcast(BcastParams p) {
+    constexpr int NT = R::kPacketThreads;
     __shared__ uint64_t s_words[1][kMaxWords];
-    const Chunk ch = chunk_of(p.d, p.L, p.cpp);
+    const Chunk ch = chunk_of<NT>(p.d, p.L, p.cpp);
     MaskSource src{false, 0, 0, p.arrived};
     const int dirs[1] = {1};
-    stage_masks(1, &src, p.n, p.P, ch.k, 0, dirs, s_words);
+    stage_masks<NT>(1, &src, p.n, p.P, ch.k, 0, dirs, s_words);
     if (ch.nv == 0) return;
     const int nw = (p.n + 63) >> 6;
     float th[8];
@@ -224,15 +227,16 @@ __global__ __launch_bounds__(kThreads) void k_broadcast(BcastParams p) {
 
 // Drift over all rows of the chunk (rows read in ascending order).
 template <class R>
-__global__ __launch_bounds__(kThreads) void k_drift(DriftParams p) {
+__global__ __launch_bounds__(R::kPacketThreads) void k_drift(DriftParams p) {
+    constexpr int NT = R::kPacketThreads;
     __shared__ uint64_t s_words[1][kMaxWords];
-    const Chunk ch = chunk_of(p.d, p.L, p.cpp);
+    const Chunk ch = chunk_of<NT>(p.d, p.L, p.cpp);
     const int nw = (p.n + 63) >> 6;
     uint32_t stale = 0;
     if (p.arrived) {
         MaskSource src{false, 0, 0, p.arrived};
         const int dirs[1] = {1};
-        stage_masks(1, &src, p.n, p.P, ch.k, 0, dirs, s_words);
+        stage_masks<NT>(1, &src, p.n, p.P, ch.k, 0, dirs, s_words);
         if (ch.c == 0) stale = (uint32_t)(p.n - popcount_words(s_words[0], nw));
     }
     const typename R::T* reps = reinterpret_cast<const typename R::T*>(p.replicas);
@@ -265,7 +269,7 @@ __global__ __launch_bounds__(kThreads) void k_drift(DriftParams p) {
         acc.finish(p.n, ch.nv, pair, range);
         abs_sum = acc.abs_sum;
     }
-    block_reduce_partial(pair, abs_sum, range, stale, 0, p.partials + blockIdx.x);
+    block_reduce_partial<NT>(pair, abs_sum, range, stale, 0, p.partials + blockIdx.x);
 }
 
 // Fixed-order reduction of the per-workgroup partials into the ll_drift
@@ -343,18 +347,19 @@ static hipError_t launch_drift_reduce(const DriftPartial* parts, int64_t count, 
 // once) and, with drift, the stale replica rows (read once).
 // ---------------------------------------------------------------------------
 template <class G, class R, bool DRIFT>
-__global__ __launch_bounds__(kThreads) void k_step_fused(FusedParams p) {
+__global__ __launch_bounds__(R::kPacketThreads) void k_step_fused(FusedParams p) {
+    constexpr int NT = R::kPacketThreads;
     __shared__ uint64_t s_words[2][kMaxWords];
-    const Chunk ch = chunk_of(p.d, p.L, p.cpp);
+    const Chunk ch = chunk_of<NT>(p.d, p.L, p.cpp);
     const int dirs[2] = {0, 1};
-    stage_masks(2, p.src, p.n, p.P, ch.k, p.step, dirs, s_words);
+    stage_masks<NT>(2, p.src, p.n, p.P, ch.k, p.step, dirs, s_words);
     const int nw = (p.n + 63) >> 6;
     const int K = popcount_words(s_words[0], nw);
     const int RC = popcount_words(s_words[1], nw);
 
     if (ch.c == 0) {
         if (threadIdx.x == 0 && p.counts) p.counts[ch.k] = K;
-        for (int i = threadIdx.x; i < p.n; i += kThreads) {
+        for (int i = threadIdx.x; i < p.n; i += NT) {
             if (p.out_g) p.out_g[(int64_t)i * p.P + ch.k] = (s_words[0][i >> 6] >> (i & 63)) & 1;
             if (p.out_b) p.out_b[(int64_t)i * p.P + ch.k] = (s_words[1][i >> 6] >> (i & 63)) & 1;
         }
@@ -422,7 +427,7 @@ __global__ __launch_bounds__(kThreads) void k_step_fused(FusedParams p) {
     if (DRIFT) {
         const uint32_t stale = ch.c == 0 ? (uint32_t)(p.n - RC) : 0u;
         const uint32_t empty = (ch.c == 0 && K == 0) ? 1u : 0u;
-        block_reduce_partial(pair, abs_sum, range, stale, empty, p.partials + blockIdx.x);
+        block_reduce_partial<NT>(pair, abs_sum, range, stale, empty, p.partials + blockIdx.x);
     }
 }
 
@@ -463,58 +468,84 @@ hipError_t launch_masks_ge(const GeLaunch& L, int ndir, hipStream_t s) {
     return hipGetLastError();
 }
 
-hipError_t launch_aggregate(int gdtype, const AggParams& p, int64_t blocks, hipStream_t s) {
-    if (gdtype == 1)
-        hipLaunchKernelGGL(k_aggregate<BF16>, dim3((unsigned)blocks), dim3(kThreads), 0, s, p);
-    else
-        hipLaunchKernelGGL(k_aggregate<F32>, dim3((unsigned)blocks), dim3(kThreads), 0, s, p);
+// Chunks per packet and workgroups for a per-packet kernel of NT threads.
+template <int NT>
+static int64_t packet_grid(int64_t P, int64_t L, int* cpp) {
+    *cpp = (int)((L + NT * kElems - 1) / (NT * kElems));
+    return P * *cpp;
+}
+
+template <class G>
+static void launch_aggregate_t(AggParams p, hipStream_t s) {
+    constexpr int NT = G::kPacketThreads;
+    const int64_t blocks = packet_grid<NT>(p.P, p.L, &p.cpp);
+    hipLaunchKernelGGL(k_aggregate<G>, dim3((unsigned)blocks), dim3(NT), 0, s, p);
+}
+
+hipError_t launch_aggregate(int gdtype, const AggParams& p, hipStream_t s) {
+    if (gdtype == 1) launch_aggregate_t<BF16>(p, s);
+    else launch_aggregate_t<F32>(p, s);
     return hipGetLastError();
 }
 
 hipError_t launch_shard_step(int64_t d, const OptParams& o, float* theta, float* m, float* v,
                              const float* g_hat, hipStream_t s) {
-    const int64_t blocks = (d + kChunk - 1) / kChunk;
+    const int64_t blocks = (d + kThreads * kElems - 1) / (kThreads * kElems);
     hipLaunchKernelGGL(k_shard_step, dim3((unsigned)blocks), dim3(kThreads), 0, s, d, o, theta,
                        m, v, g_hat);
     return hipGetLastError();
 }
 
-hipError_t launch_broadcast(int rdtype, const BcastParams& p, int64_t blocks, hipStream_t s) {
-    if (rdtype == 1)
-        hipLaunchKernelGGL(k_broadcast<BF16>, dim3((unsigned)blocks), dim3(kThreads), 0, s, p);
-    else
-        hipLaunchKernelGGL(k_broadcast<F32>, dim3((unsigned)blocks), dim3(kThreads), 0, s, p);
+template <class R>
+static void launch_broadcast_t(BcastParams p, hipStream_t s) {
+    constexpr int NT = R::kPacketThreads;
+    const int64_t blocks = packet_grid<NT>(p.P, p.L, &p.cpp);
+    hipLaunchKernelGGL(k_broadcast<R>, dim3((unsigned)blocks), dim3(NT), 0, s, p);
+}
+
+hipError_t launch_broadcast(int rdtype, const BcastParams& p, hipStream_t s) {
+    if (rdtype == 1) launch_broadcast_t<BF16>(p, s);
+    else launch_broadcast_t<F32>(p, s);
     return hipGetLastError();
 }
 
-hipError_t launch_drift(int rdtype, const DriftParams& p, int64_t blocks, int n, int64_t d,
-                        int have_master, DriftOut* out, hipStream_t s) {
-    if (rdtype == 1)
-        hipLaunchKernelGGL(k_drift<BF16>, dim3((unsigned)blocks), dim3(kThreads), 0, s, p);
-    else
-        hipLaunchKernelGGL(k_drift<F32>, dim3((unsigned)blocks), dim3(kThreads), 0, s, p);
+template <class R>
+static int64_t launch_drift_t(DriftParams p, hipStream_t s) {
+    constexpr int NT = R::kPacketThreads;
+    const int64_t blocks = packet_grid<NT>(p.P, p.L, &p.cpp);
+    hipLaunchKernelGGL(k_drift<R>, dim3((unsigned)blocks), dim3(NT), 0, s, p);
+    return blocks;
+}
+
+hipError_t launch_drift(int rdtype, const DriftParams& p, int n, int64_t d, int have_master,
+                        DriftOut* out, hipStream_t s) {
+    const int64_t blocks = rdtype == 1 ? launch_drift_t<BF16>(p, s) : launch_drift_t<F32>(p, s);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
     return launch_drift_reduce(p.partials, blocks, p.groups, n, d, have_master, out, s);
 }
 
+// The fused step's geometry follows the replica type, like the standalone
+// drift kernel, so both fold drift partials over the same partition.
 template <class G, class R>
-static void launch_fused_gr(bool drift, const FusedParams& p, int64_t blocks, hipStream_t s) {
+static int64_t launch_fused_gr(bool drift, FusedParams p, hipStream_t s) {
+    constexpr int NT = R::kPacketThreads;
+    const int64_t blocks = packet_grid<NT>(p.P, p.L, &p.cpp);
     if (drift)
-        hipLaunchKernelGGL((k_step_fused<G, R, true>), dim3((unsigned)blocks), dim3(kThreads), 0,
-                           s, p);
+        hipLaunchKernelGGL((k_step_fused<G, R, true>), dim3((unsigned)blocks), dim3(NT), 0, s, p);
     else
-        hipLaunchKernelGGL((k_step_fused<G, R, false>), dim3((unsigned)blocks), dim3(kThreads), 0,
-                           s, p);
+        hipLaunchKernelGGL((k_step_fused<G, R, false>), dim3((unsigned)blocks), dim3(NT), 0, s, p);
+    return blocks;
 }
 
-hipError_t launch_fused(int gdtype, int rdtype, const FusedParams& p, int64_t blocks,
-                        DriftOut* drift, hipStream_t s) {
+hipError_t launch_fused(int gdtype, int rdtype, const FusedParams& p, DriftOut* drift,
+                        hipStream_t s) {
     const bool dr = drift != nullptr;
-    if (gdtype == 1 && rdtype == 1) launch_fused_gr<BF16, BF16>(dr, p, blocks, s);
-    else if (gdtype == 1) launch_fused_gr<BF16, F32>(dr, p, blocks, s);
-    else if (rdtype == 1) launch_fused_gr<F32, BF16>(dr, p, blocks, s);
-    else launch_fused_gr<F32, F32>(dr, p, blocks, s);
+    int64_t blocks;
+    if (gdtype == 1 && rdtype == 1) blocks = launch_fused_gr<BF16, BF16>(dr, p, s);
+    else if (gdtype == 1) blocks = launch_fused_gr<BF16, F32>(dr, p, s);
+    else if (rdtype == 1) blocks = launch_fused_gr<F32, BF16>(dr, p, s);
+    else blocks = launch_fused_gr<F32, F32>(dr, p, s);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || !dr) return e;
     return launch_drift_reduce(p.partials, blocks, p.groups, p.n, p.d, 1, drift, s);

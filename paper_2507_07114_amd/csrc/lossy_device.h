@@ -12,9 +12,12 @@
 
 namespace lossy {
 
-constexpr int kThreads = 256;              // threads per workgroup (4 waves)
-constexpr int kElems = 8;                  // consecutive elements per thread
-constexpr int kChunk = kThreads * kElems;  // elements per workgroup
+constexpr int kThreads = 256;  // threads per workgroup of the flat kernels (4 waves)
+constexpr int kElems = 8;      // consecutive elements per thread
+// Per-packet kernels size their workgroups by the element type of the rows
+// they stream (F32::kPacketThreads, BF16::kPacketThreads): a workgroup then
+// covers 4 KiB of each row, which measured fastest for both types.
+constexpr int kMinPacketThreads = 128;
 constexpr int kMaxWorkers = 1024;
 constexpr int kMaxWords = kMaxWorkers / 64;
 constexpr int kBatchGrad = 4;   // gradient rows in flight per thread (aggregate)
@@ -68,9 +71,11 @@ __device__ __forceinline__ bool bernoulli_arrived(uint64_t k, uint64_t i, uint64
 // ---------------------------------------------------------------------------
 struct F32 {
     typedef float T;
+    static constexpr int kPacketThreads = 128;
 };
 struct BF16 {
     typedef uint16_t T;
+    static constexpr int kPacketThreads = 256;
 };
 
 __device__ __forceinline__ float bf16_to_f32(uint32_t h) { return __uint_as_float(h << 16); }
@@ -199,14 +204,15 @@ struct MaskSource {
 };
 
 // Stage the masks of packet k for `ndir` directions into words[dir][w].
-// All threads of the workgroup must call it (it ends with a barrier).
+// All NT threads of the workgroup must call it (it ends with a barrier).
+template <int NT>
 __device__ __forceinline__ void stage_masks(int ndir, const MaskSource* src, int n,
                                             int64_t num_packets, int64_t k, uint64_t step,
                                             const int* dirs,
                                             uint64_t (*words)[kMaxWords]) {
     const int nw = (n + 63) >> 6;
     const int span = nw * 64;
-    for (int idx = threadIdx.x; idx < ndir * span; idx += kThreads) {
+    for (int idx = threadIdx.x; idx < ndir * span; idx += NT) {
         const int s = idx / span;
         const int i = idx - s * span;
         bool arrived = false;
@@ -358,12 +364,13 @@ struct DriftPartial {
     uint32_t stale, empty;
 };
 
-// Fixed-order workgroup reduction of (pair, abs, range); thread 0 writes
-// the partial together with the packet bookkeeping counts.
+// Fixed-order reduction of (pair, abs, range) over a workgroup of NT
+// threads; thread 0 writes the partial with the packet bookkeeping counts.
+template <int NT>
 __device__ __forceinline__ void block_reduce_partial(double pair, double abs_sum,
                                                      double range, uint32_t stale,
                                                      uint32_t empty, DriftPartial* out) {
-    __shared__ double s_red[3][kThreads / 64];
+    __shared__ double s_red[3][NT / 64];
 #pragma unroll
     for (int off = 32; off > 0; off >>= 1) {
         pair += __shfl_down(pair, off, 64);
@@ -380,7 +387,7 @@ __device__ __forceinline__ void block_reduce_partial(double pair, double abs_sum
     __syncthreads();
     if (threadIdx.x == 0) {
         double p = 0.0, a = 0.0, r = 0.0;
-        for (int w = 0; w < kThreads / 64; ++w) {
+        for (int w = 0; w < NT / 64; ++w) {
             p += s_red[0][w];
             a += s_red[1][w];
             r = s_red[2][w] > r ? s_red[2][w] : r;

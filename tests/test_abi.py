@@ -41,7 +41,8 @@ def test_struct_layouts():
 
 
 def test_workspace_bytes_host_logic():
-    # partials: 32 B per workgroup (P * ceil(L / 2048)) and 256 second-level
+    # partials: 32 B per workgroup of the smallest geometry (P * ceil(L / 1024))
+    # and 256 second-level
     # ones of 40 B, then two n*P mask areas and the Gilbert-Elliott scan scratch of
     # both directions, each region rounded up to 256 B.
     def r256(x):
@@ -52,7 +53,7 @@ def test_workspace_bytes_host_logic():
     n, d, L = 64, 105_250_000, 4096
     P = (d + L - 1) // L
     groups = 256 * 40  # second-level drift partials
-    assert ll.ll_workspace_bytes(n, d, L) == (r256(P * 2 * 32) + groups + 2 * r256(n * P)
+    assert ll.ll_workspace_bytes(n, d, L) == (r256(P * 4 * 32) + groups + 2 * r256(n * P)
                                               + 2 * ge(n, P))
     assert ll.ll_workspace_bytes(4, 10, 8) == 256 + groups + 2 * 256 + 2 * ge(4, 2)
     assert ll.ll_masks_workspace_bytes(16, 65536) == ge(16, 65536)
