@@ -276,7 +276,7 @@ def main():
         "hbm_copy_probe_gbs": round(copy_gbs, 1),
         "roofline": {
             "bound": "hbm",
-            "kernel": "k_step_fused (+ k_drift_final)",
+            "kernel": "k_step_fused (+ k_drift_reduce, k_drift_final)",
             "achieved": round(achieved, 2),
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
