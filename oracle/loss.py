@@ -83,3 +83,20 @@ def ge_arrivals(seed: int, t: int, direction: int, n: int, num_packets: int,
         lost = u_loss[:, k] < t_loss[state]
         arrived[:, k] = np.where(lost, 0, 1)
     return arrived, state.astype(np.uint8)
+
+
+def apply_overrides(arrived: np.ndarray, owner: int = -1, reliable=None) -> np.ndarray:
+    """Transfers that never cross the lossy network.
+
+    owner >= 0: the owner's own row always arrives (its own gradient piece
+    and its own replica stay local; Section 3 step (4) broadcasts to the
+    other workers).  reliable: per-packet flags (1 = sent over a reliable
+    channel, the hybrid transport the paper's Section 5 proposes); a flagged
+    packet arrives at every row.  arrived: uint8 [n][len(reliable)].
+    """
+    out = np.array(arrived, dtype=np.uint8, copy=True)
+    if owner >= 0:
+        out[owner, :] = 1
+    if reliable is not None:
+        out[:, np.asarray(reliable).astype(bool)] = 1
+    return out

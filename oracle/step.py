@@ -63,6 +63,43 @@ def aggregate(g: np.ndarray, S: np.ndarray, lam: float, theta: np.ndarray):
     return g_hat, K.astype(np.int64), mean_abs
 
 
+def aggregate_horvitz_thompson(g: np.ndarray, S: np.ndarray, q: np.ndarray):
+    """Horvitz-Thompson form of the aggregate (one of the estimator variants
+    for unreliable delivery): every arrived contribution is weighted by the
+    inverse of its arrival probability q and the sum is divided by N, so
+    E[g_hat] = mean over all N rows with no conditioning and no fallback.
+
+    g, S, q: [n][E] (q = 1 for rows or packets that cannot be lost).
+    Returns (g_hat [E], scale [E]) with scale = sum_i S |g| / q / N.
+    """
+    n = g.shape[0]
+    S = S.astype(np.float64)
+    g_hat = (S * g / q).sum(axis=0) / n
+    scale = (S * np.abs(g) / q).sum(axis=0) / n
+    return g_hat, scale
+
+
+def aggregate_stale_fill(g: np.ndarray, S: np.ndarray, g_prev: np.ndarray):
+    """Algorithm 1's gradient half, per contribution: a lost contribution is
+    replaced by the last one that arrived from that worker for the same
+    element (g_prev, zero before the first arrival), an arrived one is used
+    and remembered; the N values are then averaged.
+
+    Returns (g_hat [E], new g_prev [n][E], scale [E] = mean |value|).
+    """
+    n = g.shape[0]
+    A = S.astype(bool)
+    vals = np.where(A, g, g_prev)
+    return vals.sum(axis=0) / n, np.where(A, g, g_prev), np.abs(vals).sum(axis=0) / n
+
+
+def update_ages(ages: np.ndarray, R: np.ndarray, cap: int = 65535) -> np.ndarray:
+    """Steps since each (replica, packet) last received the broadcast:
+    0 where it arrived this step, previous age + 1 (saturating) otherwise."""
+    a = np.asarray(ages, dtype=np.int64)
+    return np.where(np.asarray(R).astype(bool), 0, np.minimum(a + 1, cap)).astype(np.uint16)
+
+
 def sgd(theta, g_hat, lr):
     """Section 3 step (3): theta_{t+1} = theta_t - eta * g_hat."""
     return theta - lr * g_hat
@@ -93,14 +130,19 @@ def broadcast(old, new, R):
 
 def lossy_step(*, d: int, packet: int, packets, gdtype: str, grads, theta, m, v,
                replicas, arrived_g, arrived_b, opt: dict, t: int,
-               lam: float = 0.0):
+               lam: float = 0.0, estimator: str = "arrived_mean", q=None,
+               g_prev=None):
     """One step over the chosen packets.
 
     grads, replicas: [n][E] storage values for the packets' elements
     (fp32, or bf16 bit patterns); theta, m, v: [E] fp32 (m, v may be None);
     arrived_g, arrived_b: uint8 [n][len(packets)]; t: 0-based step index.
+    estimator: "arrived_mean" (Section 3 step (2)), "horvitz_thompson" (needs
+    q: arrival probabilities [n][len(packets)]) or "stale_fill" (Algorithm 1;
+    needs g_prev, storage values [n][E], returned updated).
     Returns a dict with g_hat (fp32), counts (per packet), mean_abs (per
-    element), theta, m, v (fp32) and replicas (storage dtype).
+    element: the scale of the terms summed), theta, m, v (fp32), replicas
+    (storage dtype) and g_prev (stale_fill only).
     """
     lens = packet_lengths(d, packet, packets)
     S = np.repeat(np.asarray(arrived_g), lens, axis=1)
@@ -108,7 +150,17 @@ def lossy_step(*, d: int, packet: int, packets, gdtype: str, grads, theta, m, v,
     g = widen(grads, gdtype)
     th = np.asarray(theta, dtype=np.float32).astype(np.float64)
 
-    g_hat64, _, mean_abs = aggregate(g, S, lam, th)
+    new_prev = None
+    if estimator == "arrived_mean":
+        g_hat64, _, mean_abs = aggregate(g, S, lam, th)
+    elif estimator == "horvitz_thompson":
+        Q = np.repeat(np.asarray(q, dtype=np.float64), lens, axis=1)
+        g_hat64, mean_abs = aggregate_horvitz_thompson(g, S, Q)
+    elif estimator == "stale_fill":
+        g_hat64, prev64, mean_abs = aggregate_stale_fill(g, S, widen(g_prev, gdtype))
+        new_prev = np.where(S.astype(bool), np.asarray(grads), np.asarray(g_prev))
+    else:
+        raise ValueError(f"unknown estimator {estimator!r}")
     g_hat32 = g_hat64.astype(np.float32)
     G = g_hat32.astype(np.float64)
 
@@ -134,4 +186,4 @@ def lossy_step(*, d: int, packet: int, packets, gdtype: str, grads, theta, m, v,
         g_hat=g_hat32, counts=counts, mean_abs=mean_abs, theta=theta32,
         m=None if m1 is None else m1.astype(np.float32),
         v=None if v1 is None else v1.astype(np.float32),
-        replicas=reps)
+        replicas=reps, g_prev=new_prev)
