@@ -62,6 +62,7 @@ enum { LL_F32 = 0, LL_BF16 = 1 };
 enum { LL_LOSS_BERNOULLI = 0, LL_LOSS_GILBERT_ELLIOTT = 1 };
 enum { LL_SGD = 0, LL_SGD_MOMENTUM = 1, LL_ADAM = 2 };
 enum { LL_DIR_GRAD = 0, LL_DIR_BCAST = 1 };
+enum { LL_EST_ARRIVED_MEAN = 0, LL_EST_HORVITZ_THOMPSON = 1, LL_EST_STALE_FILL = 2 };
 
 /*
  * Loss process (Section 3 steps (2) and (4): each transfer succeeds with
@@ -123,6 +124,48 @@ typedef struct {
 } ll_drift;
 
 /*
+ * Optional variants of the step; every entry point that takes `ext` accepts
+ * NULL for the defaults (all zero except owner = -1).
+ *   estimator  how the owner combines a packet's contributions:
+ *     LL_EST_ARRIVED_MEAN      (default) sum of the arrived contributions over
+ *                              their count (Section 3 step (2)); fallback when
+ *                              none arrived (see ll_opt.fallback_lambda).
+ *     LL_EST_HORVITZ_THOMPSON  each arrived contribution weighted by 1/q and
+ *                              the sum divided by N: unbiased with no
+ *                              conditioning and no fallback.  q = arrival_prob
+ *                              for lossy contributions and 1 for those that
+ *                              cannot be lost (owner row, reliable packets).
+ *     LL_EST_STALE_FILL        Algorithm 1's gradient half: a lost contribution
+ *                              is replaced by the last one that arrived from
+ *                              that worker (g_prev), an arrived one is used and
+ *                              stored into g_prev; the N values are averaged.
+ *   owner         -1, or the row whose gradient piece and replica stay local
+ *                 (Section 3 step (4) broadcasts to the other workers): that
+ *                 row always arrives, in both directions.
+ *   reliable      uint8 [P] (device) or NULL: packets flagged 1 travel over a
+ *                 reliable channel (the hybrid transport proposed in the
+ *                 paper's Section 5) and arrive at every row, both directions.
+ *   g_prev        [n][ld_g] of the gradient dtype (device, in/out), required by
+ *                 LL_EST_STALE_FILL (zero before the first step), else unused.
+ *   ages          uint16 [n][P] (device, in/out) or NULL; lossy_step_fused only:
+ *                 steps since each replica packet last received the broadcast
+ *                 (0 = this step; saturates at 65535).
+ *   arrival_prob  q of LL_EST_HORVITZ_THOMPSON in (0, 1].  lossy_aggregate
+ *                 requires it; lossy_step_fused takes 0 to mean 1 - p of a
+ *                 Bernoulli gradient loss.
+ * Masks read from memory (lossy_aggregate, lossy_broadcast, drift_stats) are
+ * taken as given: ll_masks and lossy_step_fused apply owner and reliable.
+ */
+typedef struct {
+    int32_t estimator;
+    int32_t owner;
+    const uint8_t* reliable;
+    void* g_prev;
+    uint16_t* ages;
+    double arrival_prob;
+} ll_ext;
+
+/*
  * Arrival masks for one step and direction (Section 3 step (2) for
  * dir = LL_DIR_GRAD, step (4) for LL_DIR_BCAST) under `loss` (host).
  *   n, num_packets   mask shape [n][num_packets]; arrived (device, out).
@@ -134,10 +177,11 @@ typedef struct {
  *   workspace        Gilbert-Elliott only: device scratch of ws_bytes >=
  *                    ll_masks_workspace_bytes(n, num_packets); ignored (may be
  *                    NULL) for Bernoulli.
+ *   ext              NULL, or variants: owner and reliable force arrivals.
  */
 LL_API int ll_masks(int32_t n, int64_t num_packets, uint64_t step, int32_t dir,
                     const ll_loss* loss, uint8_t* ge_state, uint8_t* arrived,
-                    void* workspace, size_t ws_bytes, void* stream);
+                    void* workspace, size_t ws_bytes, const ll_ext* ext, void* stream);
 
 /* Scratch bytes ll_masks needs for a Gilbert-Elliott process (0 on invalid
  * sizes).  Bernoulli masks need none. */
@@ -152,12 +196,22 @@ LL_API size_t ll_masks_workspace_bytes(int32_t n, int64_t num_packets);
  *   arrived  uint8 [n][P].
  *   theta    fp32 [d]; read only when fallback_lambda != 0 (else may be NULL).
  *   g_hat    fp32 [d] (out).  counts: int32 [P] (out, may be NULL).
- * Lost rows are never read.
+ *   ext      NULL, or the estimator variant (with owner and reliable naming
+ *            the contributions that could not be lost, and g_prev).
+ * Lost rows are never read (their g_prev is, under LL_EST_STALE_FILL).
  */
 LL_API int lossy_aggregate(int32_t n, int64_t d, int64_t packet, int32_t gdtype,
                     const void* grads, int64_t ld_g, const uint8_t* arrived,
                     float fallback_lambda, const float* theta, float* g_hat,
-                    int32_t* counts, void* stream);
+                    int32_t* counts, const ll_ext* ext, void* stream);
+
+/*
+ * Broadcast ages (see ll_ext.ages) after a broadcast with masks arrived_bc
+ * uint8 [n][num_packets]: ages[i][k] = 0 where the packet arrived, else
+ * min(ages[i][k] + 1, 65535).  ages: uint16 [n][num_packets], in/out.
+ */
+LL_API int ll_ages_update(int32_t n, int64_t num_packets, const uint8_t* arrived_bc,
+                          uint16_t* ages, void* stream);
 
 /*
  * Owner update of the fp32 master shard (Section 3 step (3)), in place.
@@ -198,7 +252,8 @@ LL_API int drift_stats(int32_t n, int64_t d, int64_t packet, int32_t rdtype,
  * replicas after the broadcast.  Equivalent to
  *   ll_masks(GRAD) -> lossy_aggregate -> shard_step -> ll_masks(BCAST)
  *   -> lossy_broadcast -> drift_stats
- * with the same arithmetic, so its outputs are bit-identical to that chain.
+ * (and ll_ages_update) with the same arithmetic, so its outputs are
+ * bit-identical to that chain.
  *   loss_g, loss_b, opt     host structs.
  *   ge_state_g, ge_state_b  uint8 [n] each (device, in/out) for
  *                           Gilbert-Elliott processes, else may be NULL.
@@ -207,6 +262,8 @@ LL_API int drift_stats(int32_t n, int64_t d, int64_t packet, int32_t rdtype,
  *   workspace, ws_bytes     scratch, ws_bytes >= ll_workspace_bytes(n, d, packet);
  *                           required with drift or a Gilbert-Elliott process.
  *   drift                   ll_drift (device, out) or NULL to skip drift.
+ *   ext                     NULL, or variants (estimator, owner, reliable,
+ *                           g_prev, ages).
  * Lost gradient packets are never read; lost broadcast packets are read only
  * for drift and never written.
  */
@@ -218,7 +275,7 @@ LL_API int lossy_step_fused(int32_t n, int64_t d, int64_t packet, uint64_t step,
                      int32_t rdtype, void* replicas, int64_t ld_r,
                      uint8_t* arrived_g, uint8_t* arrived_b, int32_t* counts,
                      void* workspace, size_t ws_bytes, ll_drift* drift,
-                     void* stream);
+                     const ll_ext* ext, void* stream);
 
 /* Bytes of device workspace that drift_stats and lossy_step_fused need for
  * these sizes (0 on invalid sizes): drift partials, two mask areas and the

@@ -18,7 +18,7 @@ import torch
 
 __all__ = [
     "LossSpec", "OptSpec", "bernoulli", "gilbert_elliott", "sgd", "sgd_momentum", "adam",
-    "ll_masks", "lossy_aggregate", "shard_step", "lossy_broadcast", "drift_stats",
+    "ll_masks", "ll_ages_update", "lossy_aggregate", "Ext", "ext", "ESTIMATORS", "shard_step", "lossy_broadcast", "drift_stats",
     "lossy_step_fused", "ll_workspace_bytes", "ll_masks_workspace_bytes", "ll_last_error",
     "drift_buffer",
     "read_drift", "library_path", "LossyError",
@@ -30,6 +30,9 @@ LL_F32, LL_BF16 = 0, 1
 LL_LOSS_BERNOULLI, LL_LOSS_GILBERT_ELLIOTT = 0, 1
 LL_SGD, LL_SGD_MOMENTUM, LL_ADAM = 0, 1, 2
 LL_DIR_GRAD, LL_DIR_BCAST = 0, 1
+LL_EST_ARRIVED_MEAN, LL_EST_HORVITZ_THOMPSON, LL_EST_STALE_FILL = 0, 1, 2
+ESTIMATORS = {"arrived_mean": LL_EST_ARRIVED_MEAN, "horvitz_thompson": LL_EST_HORVITZ_THOMPSON,
+              "stale_fill": LL_EST_STALE_FILL}
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
 
@@ -54,6 +57,30 @@ class OptSpec(ctypes.Structure):
     _fields_ = [("kind", ctypes.c_int32), ("lr", ctypes.c_float), ("momentum", ctypes.c_float),
                 ("beta1", ctypes.c_float), ("beta2", ctypes.c_float), ("eps", ctypes.c_float),
                 ("fallback_lambda", ctypes.c_float)]
+
+
+class Ext(ctypes.Structure):
+    """ll_ext: variants of the step (see include/lossy.h).  Built by ext(),
+    which also keeps the tensors behind its device pointers alive."""
+    _fields_ = [("estimator", ctypes.c_int32), ("owner", ctypes.c_int32),
+                ("reliable", ctypes.c_void_p), ("g_prev", ctypes.c_void_p),
+                ("ages", ctypes.c_void_p), ("arrival_prob", ctypes.c_double)]
+
+
+def ext(estimator: str = "arrived_mean", owner: int = -1,
+        reliable: Optional[torch.Tensor] = None, g_prev: Optional[torch.Tensor] = None,
+        ages: Optional[torch.Tensor] = None, arrival_prob: float = 0.0) -> Ext:
+    if estimator not in ESTIMATORS:
+        raise ValueError(f"unknown estimator {estimator!r}")
+    e = Ext(ESTIMATORS[estimator], owner, _flat(reliable, "reliable", torch.uint8),
+            None if g_prev is None else _rows(g_prev, "g_prev")[0],
+            _flat(ages, "ages", torch.int16), arrival_prob)
+    e._tensors = (reliable, g_prev, ages)  # the pointers above stay valid while e lives
+    return e
+
+
+def _ext_ref(e: Optional[Ext]):
+    return None if e is None else ctypes.byref(e)
 
 
 def bernoulli(p: float, seed: int = 0) -> LossSpec:
@@ -83,10 +110,11 @@ _vp = ctypes.c_void_p
 _i32, _i64, _u64, _f32 = ctypes.c_int32, ctypes.c_int64, ctypes.c_uint64, ctypes.c_float
 _SIGNATURES = {
     "ll_masks": (ctypes.c_int, [_i32, _i64, _u64, _i32, ctypes.POINTER(LossSpec), _vp, _vp, _vp,
-                                ctypes.c_size_t, _vp]),
+                                ctypes.c_size_t, ctypes.POINTER(Ext), _vp]),
+    "ll_ages_update": (ctypes.c_int, [_i32, _i64, _vp, _vp, _vp]),
     "ll_masks_workspace_bytes": (ctypes.c_size_t, [_i32, _i64]),
     "lossy_aggregate": (ctypes.c_int, [_i32, _i64, _i64, _i32, _vp, _i64, _vp, _f32, _vp, _vp,
-                                       _vp, _vp]),
+                                       _vp, ctypes.POINTER(Ext), _vp]),
     "shard_step": (ctypes.c_int, [ctypes.POINTER(OptSpec), _i64, _u64, _vp, _vp, _vp, _vp, _vp]),
     "lossy_broadcast": (ctypes.c_int, [_i32, _i64, _i64, _vp, _i32, _vp, _i64, _vp, _vp]),
     "drift_stats": (ctypes.c_int, [_i32, _i64, _i64, _i32, _vp, _i64, _vp, _vp, _vp,
@@ -94,7 +122,8 @@ _SIGNATURES = {
     "lossy_step_fused": (ctypes.c_int, [_i32, _i64, _i64, _u64, ctypes.POINTER(LossSpec),
                                         ctypes.POINTER(LossSpec), _vp, _vp, _i32, _vp, _i64,
                                         ctypes.POINTER(OptSpec), _vp, _vp, _vp, _i32, _vp, _i64,
-                                        _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp, _vp]),
+                                        _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp,
+                                        ctypes.POINTER(Ext), _vp]),
     "ll_workspace_bytes": (ctypes.c_size_t, [_i32, _i64, _i64]),
     "ll_last_error": (ctypes.c_char_p, []),
 }
@@ -168,12 +197,20 @@ def _flat(t: Optional[torch.Tensor], name: str, dtype) -> Optional[int]:
 
 def ll_masks(n: int, num_packets: int, step: int, direction: int, loss: LossSpec,
              arrived: torch.Tensor, ge_state: Optional[torch.Tensor] = None,
-             workspace: Optional[torch.Tensor] = None) -> None:
+             workspace: Optional[torch.Tensor] = None, ext: Optional[Ext] = None) -> None:
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     _check("ll_masks", _load().ll_masks(
         n, num_packets, step, direction, ctypes.byref(loss),
         _flat(ge_state, "ge_state", torch.uint8), _flat(arrived, "arrived", torch.uint8),
-        _dev(workspace, "workspace"), ws_bytes, _stream()))
+        _dev(workspace, "workspace"), ws_bytes, _ext_ref(ext), _stream()))
+
+
+def ll_ages_update(arrived_bc: torch.Tensor, ages: torch.Tensor) -> None:
+    """ages (int16 storage of uint16 counts) [n][P] after a broadcast."""
+    n, P = arrived_bc.shape
+    _check("ll_ages_update", _load().ll_ages_update(
+        n, P, _flat(arrived_bc, "arrived_bc", torch.uint8), _flat(ages, "ages", torch.int16),
+        _stream()))
 
 
 def ll_masks_workspace_bytes(n: int, num_packets: int) -> int:
@@ -183,12 +220,13 @@ def ll_masks_workspace_bytes(n: int, num_packets: int) -> int:
 def lossy_aggregate(grads: torch.Tensor, arrived: torch.Tensor, *, d: int, packet: int,
                     g_hat: torch.Tensor, fallback_lambda: float = 0.0,
                     theta: Optional[torch.Tensor] = None,
-                    counts: Optional[torch.Tensor] = None) -> None:
+                    counts: Optional[torch.Tensor] = None, ext: Optional[Ext] = None) -> None:
     gp, ld, gt = _rows(grads, "grads")
     _check("lossy_aggregate", _load().lossy_aggregate(
         grads.shape[0], d, packet, gt, gp, ld, _flat(arrived, "arrived", torch.uint8),
         fallback_lambda, _flat(theta, "theta", torch.float32),
-        _flat(g_hat, "g_hat", torch.float32), _flat(counts, "counts", torch.int32), _stream()))
+        _flat(g_hat, "g_hat", torch.float32), _flat(counts, "counts", torch.int32),
+        _ext_ref(ext), _stream()))
 
 
 def shard_step(opt: OptSpec, step: int, theta: torch.Tensor, g_hat: torch.Tensor,
@@ -244,7 +282,7 @@ def lossy_step_fused(*, d: int, packet: int, step: int, loss_g: LossSpec, loss_b
                      arrived_b: Optional[torch.Tensor] = None,
                      counts: Optional[torch.Tensor] = None,
                      workspace: Optional[torch.Tensor] = None,
-                     drift: Optional[torch.Tensor] = None) -> None:
+                     drift: Optional[torch.Tensor] = None, ext: Optional[Ext] = None) -> None:
     gp, ldg, gt = _rows(grads, "grads")
     rp, ldr, rt = _rows(replicas, "replicas")
     if replicas.shape[0] != grads.shape[0]:
@@ -257,4 +295,4 @@ def lossy_step_fused(*, d: int, packet: int, step: int, loss_g: LossSpec, loss_b
         _flat(m, "m", torch.float32), _flat(v, "v", torch.float32), rt, rp, ldr,
         _flat(arrived_g, "arrived_g", torch.uint8), _flat(arrived_b, "arrived_b", torch.uint8),
         _flat(counts, "counts", torch.int32), _dev(workspace, "workspace"), ws_bytes,
-        _dev(drift, "drift", torch.float64), _stream()))
+        _dev(drift, "drift", torch.float64), _ext_ref(ext), _stream()))

@@ -176,6 +176,49 @@ WsLayout ws_layout(int32_t n, const Geometry& g) {
     return w;
 }
 
+// Variants of the step (ll_ext), validated; defaults when ext is NULL.
+struct ExtView {
+    int est = LL_EST_ARRIVED_MEAN;
+    int owner = -1;
+    const uint8_t* reliable = nullptr;
+    void* g_prev = nullptr;
+    uint16_t* ages = nullptr;
+    double q = 0.0;
+};
+
+int read_ext(const ll_ext* e, int32_t n, ExtView* v) {
+    if (!e) return LL_OK;
+    if (e->estimator != LL_EST_ARRIVED_MEAN && e->estimator != LL_EST_HORVITZ_THOMPSON &&
+        e->estimator != LL_EST_STALE_FILL)
+        return fail(LL_EINVAL, "unknown estimator %d", e->estimator);
+    if (e->owner < -1 || e->owner >= n) return fail(LL_EINVAL, "owner=%d outside [-1, n)", e->owner);
+    if (!(e->arrival_prob >= 0.0 && e->arrival_prob <= 1.0))
+        return fail(LL_EINVAL, "arrival_prob outside [0, 1]");
+    v->est = e->estimator;
+    v->owner = e->owner;
+    v->reliable = e->reliable;
+    v->g_prev = e->g_prev;
+    v->ages = e->ages;
+    v->q = e->arrival_prob;
+    return LL_OK;
+}
+
+// Aggregation variant for the kernels; q is the Horvitz-Thompson arrival
+// probability already resolved by the caller.
+int make_variant(const ExtView& x, double q, const void* g_prev_checked, AggVariant* v) {
+    v->kind = x.est;
+    v->owner = x.owner;
+    v->reliable = x.reliable;
+    v->g_prev = const_cast<void*>(g_prev_checked);
+    v->invq = 1.0f;
+    if (x.est == LL_EST_HORVITZ_THOMPSON) {
+        if (!(q > 0.0 && q <= 1.0))
+            return fail(LL_EINVAL, "Horvitz-Thompson needs an arrival probability in (0, 1]");
+        v->invq = (float)(1.0 / q);
+    }
+    return LL_OK;
+}
+
 // Fill one direction's Gilbert-Elliott job with its scratch carved from `base`.
 GeJob make_ge_job(const ll_loss* l, int dir, uint8_t* state, uint8_t* arrived,
                   const GeScratch& gs, uint8_t* base) {
@@ -187,6 +230,8 @@ GeJob make_ge_job(const ll_loss* l, int dir, uint8_t* state, uint8_t* arrived,
     j.tmaps = base;
     j.comps = base + gs.tmaps;
     j.state_in = base + gs.tmaps + gs.comps;
+    j.owner = -1;
+    j.reliable = nullptr;
     return j;
 }
 
@@ -209,12 +254,14 @@ size_t ll_masks_workspace_bytes(int32_t n, int64_t num_packets) {
 
 int ll_masks(int32_t n, int64_t num_packets, uint64_t step, int32_t dir, const ll_loss* loss,
              uint8_t* ge_state, uint8_t* arrived, void* workspace, size_t ws_bytes,
-             void* stream) {
+             const ll_ext* ext, void* stream) {
     if (n < 1 || n > kMaxWorkers) return fail(LL_EINVAL, "n=%d outside [1, %d]", n, kMaxWorkers);
     if (num_packets < 0) return fail(LL_EINVAL, "num_packets is negative");
     if (dir != LL_DIR_GRAD && dir != LL_DIR_BCAST) return fail(LL_EINVAL, "unknown direction %d", dir);
     int r = check_loss("loss", loss);
     if (r) return r;
+    ExtView x;
+    if ((r = read_ext(ext, n, &x))) return r;
     if (!arrived) return fail(LL_EINVAL, "arrived is NULL");
     const bool ge = loss->kind == LL_LOSS_GILBERT_ELLIOTT;
     if (ge && !ge_state) return fail(LL_EINVAL, "ge_state is NULL for a Gilbert-Elliott process");
@@ -226,7 +273,8 @@ int ll_masks(int32_t n, int64_t num_packets, uint64_t step, int32_t dir, const l
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     if (!ge)
         return hip_check(launch_masks_bernoulli(n, num_packets, step, dir, loss->seed,
-                                                threshold(loss->p), arrived, s),
+                                                threshold(loss->p), x.owner, x.reliable, arrived,
+                                                s),
                          "ll_masks");
     GeLaunch L;
     L.n = n;
@@ -234,13 +282,16 @@ int ll_masks(int32_t n, int64_t num_packets, uint64_t step, int32_t dir, const l
     L.S = gs.S;
     L.step = step;
     L.job[0] = make_ge_job(loss, dir, ge_state, arrived, gs, reinterpret_cast<uint8_t*>(workspace));
+    L.job[0].owner = x.owner;
+    L.job[0].reliable = x.reliable;
     L.job[1] = L.job[0];
     return hip_check(launch_masks_ge(L, 1, s), "ll_masks");
 }
 
 int lossy_aggregate(int32_t n, int64_t d, int64_t packet, int32_t gdtype, const void* grads,
                     int64_t ld_g, const uint8_t* arrived, float fallback_lambda,
-                    const float* theta, float* g_hat, int32_t* counts, void* stream) {
+                    const float* theta, float* g_hat, int32_t* counts, const ll_ext* ext,
+                    void* stream) {
     Geometry g;
     int r = check_shape(n, d, packet, &g);
     if (r) return r;
@@ -250,7 +301,11 @@ int lossy_aggregate(int32_t n, int64_t d, int64_t packet, int32_t gdtype, const 
     if (!arrived) return fail(LL_EINVAL, "arrived is NULL");
     if ((r = check_vec("g_hat", g_hat, true))) return r;
     if ((r = check_vec("theta", theta, fallback_lambda != 0.0f))) return r;
+    ExtView x;
+    if ((r = read_ext(ext, n, &x))) return r;
+    if (x.est == LL_EST_STALE_FILL && (r = check_rows("g_prev", x.g_prev, ld_g, d))) return r;
     AggParams p;
+    if ((r = make_variant(x, x.q, x.g_prev, &p.var))) return r;
     p.n = n;
     p.d = d;
     p.L = packet;
@@ -265,6 +320,18 @@ int lossy_aggregate(int32_t n, int64_t d, int64_t packet, int32_t gdtype, const 
     p.counts = counts;
     return hip_check(launch_aggregate(gdtype, p, reinterpret_cast<hipStream_t>(stream)),
                      "lossy_aggregate");
+}
+
+int ll_ages_update(int32_t n, int64_t num_packets, const uint8_t* arrived_bc, uint16_t* ages,
+                   void* stream) {
+    if (n < 1 || n > kMaxWorkers) return fail(LL_EINVAL, "n=%d outside [1, %d]", n, kMaxWorkers);
+    if (num_packets < 0) return fail(LL_EINVAL, "num_packets is negative");
+    if (num_packets == 0) return ok();
+    if (!arrived_bc) return fail(LL_EINVAL, "arrived_bc is NULL");
+    if (!ages) return fail(LL_EINVAL, "ages is NULL");
+    return hip_check(launch_ages_update((int64_t)n * num_packets, arrived_bc, ages,
+                                        reinterpret_cast<hipStream_t>(stream)),
+                     "ll_ages_update");
 }
 
 int shard_step(const ll_opt* opt, int64_t d, uint64_t step, float* theta, float* m, float* v,
@@ -346,7 +413,8 @@ int lossy_step_fused(int32_t n, int64_t d, int64_t packet, uint64_t step, const 
                      int32_t gdtype, const void* grads, int64_t ld_g, const ll_opt* opt,
                      float* theta, float* m, float* v, int32_t rdtype, void* replicas,
                      int64_t ld_r, uint8_t* arrived_g, uint8_t* arrived_b, int32_t* counts,
-                     void* workspace, size_t ws_bytes, ll_drift* drift, void* stream) {
+                     void* workspace, size_t ws_bytes, ll_drift* drift, const ll_ext* ext,
+                     void* stream) {
     Geometry g;
     int r = check_shape(n, d, packet, &g);
     if (r) return r;
@@ -354,6 +422,8 @@ int lossy_step_fused(int32_t n, int64_t d, int64_t packet, uint64_t step, const 
     if ((r = check_loss("loss_b", loss_b))) return r;
     if ((r = check_dtype("gdtype", gdtype))) return r;
     if ((r = check_dtype("rdtype", rdtype))) return r;
+    ExtView x;
+    if ((r = read_ext(ext, n, &x))) return r;
     const bool ge_g = loss_g->kind == LL_LOSS_GILBERT_ELLIOTT;
     const bool ge_b = loss_b->kind == LL_LOSS_GILBERT_ELLIOTT;
     if (ge_g && !ge_state_g) return fail(LL_EINVAL, "ge_state_g is NULL for a Gilbert-Elliott process");
@@ -369,6 +439,15 @@ int lossy_step_fused(int32_t n, int64_t d, int64_t packet, uint64_t step, const 
     if ((r = check_vec("theta", theta, true))) return r;
     OptParams o;
     if ((r = make_opt(opt, step, m, v, &o))) return r;
+    if (x.est == LL_EST_STALE_FILL && (r = check_rows("g_prev", x.g_prev, ld_g, d))) return r;
+    double q = x.q;
+    if (x.est == LL_EST_HORVITZ_THOMPSON && q == 0.0) {
+        if (loss_g->kind != LL_LOSS_BERNOULLI)
+            return fail(LL_EINVAL, "Horvitz-Thompson under Gilbert-Elliott loss needs arrival_prob");
+        q = 1.0 - loss_g->p;
+    }
+    AggVariant var;
+    if ((r = make_variant(x, q, x.g_prev, &var))) return r;
     const WsLayout w = ws_layout(n, g);
     const bool need_ws = drift || ge_g || ge_b;
     if (need_ws) {
@@ -399,6 +478,8 @@ int lossy_step_fused(int32_t n, int64_t d, int64_t packet, uint64_t step, const 
     p.ld_r = ld_r;
     p.partials = drift ? reinterpret_cast<DriftPartial*>(ws) : nullptr;
     p.groups = drift ? reinterpret_cast<DriftAcc*>(ws + w.groups_off) : nullptr;
+    p.var = var;
+    p.ages = x.ages;
 
     const ll_loss* losses[2] = {loss_g, loss_b};
     uint8_t* states[2] = {ge_state_g, ge_state_b};
@@ -412,13 +493,16 @@ int lossy_step_fused(int32_t n, int64_t d, int64_t packet, uint64_t step, const 
     for (int dir = 0; dir < 2; ++dir) {
         const ll_loss* l = losses[dir];
         if (l->kind == LL_LOSS_BERNOULLI) {
-            p.src[dir] = MaskSource{true, l->seed, threshold(l->p), nullptr};
+            p.src[dir] = MaskSource{true, l->seed, threshold(l->p), nullptr, x.owner, x.reliable};
         } else {
             // Sequential chain: the scan writes the masks, the step reads them.
             uint8_t* dst = outs[dir] ? outs[dir] : ws + w.partials + dir * w.masks;
-            L.job[nge++] = make_ge_job(l, dir, states[dir], dst, w.gs,
-                                       ws + w.partials + 2 * w.masks + dir * w.gs.per_dir);
-            p.src[dir] = MaskSource{false, 0, 0, dst};
+            L.job[nge] = make_ge_job(l, dir, states[dir], dst, w.gs,
+                                     ws + w.partials + 2 * w.masks + dir * w.gs.per_dir);
+            L.job[nge].owner = x.owner;
+            L.job[nge].reliable = x.reliable;
+            ++nge;
+            p.src[dir] = MaskSource{false, 0, 0, dst, -1, nullptr};
             if (dir == 0) p.out_g = nullptr;  // already written by the scan
             else p.out_b = nullptr;
         }

@@ -60,6 +60,8 @@ struct GeJob {
     uint8_t* tmaps;     // [n][S][kThreads] per-run composite maps (scratch)
     uint8_t* comps;     // [n][S] per-segment composite maps (scratch)
     uint8_t* state_in;  // [n] copy of the input state (scratch)
+    int owner;                // row that always arrives, or -1
+    const uint8_t* reliable;  // [P] packets that always arrive, or null
 };
 
 struct GeLaunch {
@@ -80,6 +82,7 @@ struct AggParams {
     const float* theta;
     float* g_hat;
     int32_t* counts;
+    AggVariant var;
 };
 
 struct BcastParams {
@@ -124,10 +127,15 @@ struct FusedParams {
     int64_t ld_r;
     DriftPartial* partials;
     DriftAcc* groups;  // [kReduceGroups] second-level partials
+    AggVariant var;
+    uint16_t* ages;    // [n][P] broadcast ages, or null
 };
 
 hipError_t launch_masks_bernoulli(int n, int64_t num_packets, uint64_t step, int dir,
-                                  uint64_t seed, uint64_t thr, uint8_t* arrived, hipStream_t s);
+                                  uint64_t seed, uint64_t thr, int owner,
+                                  const uint8_t* reliable, uint8_t* arrived, hipStream_t s);
+hipError_t launch_ages_update(int64_t total, const uint8_t* arrived, uint16_t* ages,
+                              hipStream_t s);
 hipError_t launch_masks_ge(const GeLaunch& L, int ndir, hipStream_t s);
 hipError_t launch_aggregate(int gdtype, const AggParams& p, hipStream_t s);
 hipError_t launch_shard_step(int64_t d, const OptParams& o, float* theta, float* m, float* v,

@@ -20,13 +20,16 @@ namespace lossy {
 __global__ __launch_bounds__(kThreads) void k_masks_bernoulli(int n, int64_t num_packets,
                                                               uint64_t step, uint64_t dir,
                                                               uint64_t seed, uint64_t thr,
+                                                              int owner, const uint8_t* reliable,
                                                               uint8_t* arrived) {
     const int64_t total = (int64_t)n * num_packets;
     for (int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x; idx < total;
          idx += (int64_t)gridDim.x * kThreads) {
         const int64_t i = idx / num_packets;
         const int64_t k = idx - i * num_packets;
-        arrived[idx] = bernoulli_arrived((uint64_t)k, (uint64_t)i, step, dir, seed, thr) ? 1 : 0;
+        const bool a = bernoulli_arrived((uint64_t)k, (uint64_t)i, step, dir, seed, thr) ||
+                       forced_arrival((int)i, k, owner, reliable);
+        arrived[idx] = a ? 1 : 0;
     }
 }
 
@@ -131,7 +134,8 @@ __global__ __launch_bounds__(kThreads) void k_ge_apply(GeLaunch L) {
         philox4x64_10((uint64_t)k, (uint64_t)b.i, L.step, J.dir, J.ge.seed, 0, w0, w1);
         x = ge_apply(ge_packet_map(w0 >> 32, J.ge), x);
         const bool lost = (w1 >> 32) < (x ? J.ge.thr_loss_bad : J.ge.thr_loss_good);
-        J.arrived[(int64_t)b.i * L.P + k] = lost ? 0 : 1;
+        const bool a = !lost || forced_arrival(b.i, k, J.owner, J.reliable);
+        J.arrived[(int64_t)b.i * L.P + k] = a ? 1 : 0;
     }
     if (b.s == L.S - 1 && threadIdx.x == kThreads - 1) J.state[b.i] = (uint8_t)x;
 }
@@ -168,7 +172,7 @@ __global__ __launch_bounds__(G::kPacketThreads) void k_aggregate(AggParams p) {
     constexpr int NT = G::kPacketThreads;
     __shared__ uint64_t s_words[1][kMaxWords];
     const Chunk ch = chunk_of<NT>(p.d, p.L, p.cpp);
-    MaskSource src{false, 0, 0, p.arrived};
+    MaskSource src{false, 0, 0, p.arrived, -1, nullptr};
     const int dirs[1] = {0};
     stage_masks<NT>(1, &src, p.n, p.P, ch.k, 0, dirs, s_words);
     const int nw = (p.n + 63) >> 6;
@@ -176,10 +180,12 @@ __global__ __launch_bounds__(G::kPacketThreads) void k_aggregate(AggParams p) {
     if (ch.c == 0 && threadIdx.x == 0 && p.counts) p.counts[ch.k] = K;
     if (ch.nv == 0) return;
     float th[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-    if (K == 0 && p.lam != 0.0f) load_f32x8(p.theta + ch.e0, ch.nv, th);
+    if (K == 0 && p.lam != 0.0f && p.var.kind == kEstArrivedMean)
+        load_f32x8(p.theta + ch.e0, ch.nv, th);
+    const bool relp = p.var.reliable != nullptr && p.var.reliable[ch.k] != 0;
     float g[8];
     aggregate8<G>(reinterpret_cast<const typename G::T*>(p.grads), p.ld, ch.e0, ch.nv,
-                  s_words[0], nw, K, p.lam, th, g);
+                  s_words[0], nw, p.n, K, p.lam, th, p.var, relp, g);
     store_f32x8(p.g_hat + ch.e0, ch.nv, g);
 }
 
@@ -205,7 +211,7 @@ __global__ __launch_bounds__(R::kPacketThreads) void k_broadcast(BcastParams p) 
     constexpr int NT = R::kPacketThreads;
     __shared__ uint64_t s_words[1][kMaxWords];
     const Chunk ch = chunk_of<NT>(p.d, p.L, p.cpp);
-    MaskSource src{false, 0, 0, p.arrived};
+    MaskSource src{false, 0, 0, p.arrived, -1, nullptr};
     const int dirs[1] = {1};
     stage_masks<NT>(1, &src, p.n, p.P, ch.k, 0, dirs, s_words);
     if (ch.nv == 0) return;
@@ -234,7 +240,7 @@ __global__ __launch_bounds__(R::kPacketThreads) void k_drift(DriftParams p) {
     const int nw = (p.n + 63) >> 6;
     uint32_t stale = 0;
     if (p.arrived) {
-        MaskSource src{false, 0, 0, p.arrived};
+        MaskSource src{false, 0, 0, p.arrived, -1, nullptr};
         const int dirs[1] = {1};
         stage_masks<NT>(1, &src, p.n, p.P, ch.k, 0, dirs, s_words);
         if (ch.c == 0) stale = (uint32_t)(p.n - popcount_words(s_words[0], nw));
@@ -360,8 +366,11 @@ __global__ __launch_bounds__(R::kPacketThreads) void k_step_fused(FusedParams p)
     if (ch.c == 0) {
         if (threadIdx.x == 0 && p.counts) p.counts[ch.k] = K;
         for (int i = threadIdx.x; i < p.n; i += NT) {
-            if (p.out_g) p.out_g[(int64_t)i * p.P + ch.k] = (s_words[0][i >> 6] >> (i & 63)) & 1;
-            if (p.out_b) p.out_b[(int64_t)i * p.P + ch.k] = (s_words[1][i >> 6] >> (i & 63)) & 1;
+            const int64_t at = (int64_t)i * p.P + ch.k;
+            const uint8_t rb = (s_words[1][i >> 6] >> (i & 63)) & 1;
+            if (p.out_g) p.out_g[at] = (s_words[0][i >> 6] >> (i & 63)) & 1;
+            if (p.out_b) p.out_b[at] = rb;
+            if (p.ages) p.ages[at] = rb ? 0 : (p.ages[at] == 0xFFFF ? 0xFFFF : p.ages[at] + 1);
         }
     }
 
@@ -371,8 +380,9 @@ __global__ __launch_bounds__(R::kPacketThreads) void k_step_fused(FusedParams p)
         load_f32x8(p.theta + ch.e0, ch.nv, th);
         if (p.opt.kind >= 1) load_f32x8(p.m + ch.e0, ch.nv, mm);
         if (p.opt.kind == 2) load_f32x8(p.v + ch.e0, ch.nv, vv);
+        const bool relp = p.var.reliable != nullptr && p.var.reliable[ch.k] != 0;
         aggregate8<G>(reinterpret_cast<const typename G::T*>(p.grads), p.ld_g, ch.e0, ch.nv,
-                      s_words[0], nw, K, p.lam, th, g);
+                      s_words[0], nw, p.n, K, p.lam, th, p.var, relp, g);
         update8(p.opt, th, mm, vv, g);
         store_f32x8(p.theta + ch.e0, ch.nv, th);
         if (p.opt.kind >= 1) store_f32x8(p.m + ch.e0, ch.nv, mm);
@@ -450,12 +460,29 @@ __global__ void k_drift_zero(DriftOut* out) {
 static int64_t grid_cap(int64_t blocks) { return blocks < (1ll << 20) ? blocks : (1ll << 20); }
 
 hipError_t launch_masks_bernoulli(int n, int64_t num_packets, uint64_t step, int dir,
-                                  uint64_t seed, uint64_t thr, uint8_t* arrived,
-                                  hipStream_t s) {
+                                  uint64_t seed, uint64_t thr, int owner,
+                                  const uint8_t* reliable, uint8_t* arrived, hipStream_t s) {
     const int64_t total = (int64_t)n * num_packets;
     const int64_t blocks = grid_cap((total + kThreads - 1) / kThreads);
     hipLaunchKernelGGL(k_masks_bernoulli, dim3((unsigned)blocks), dim3(kThreads), 0, s, n,
-                       num_packets, step, (uint64_t)dir, seed, thr, arrived);
+                       num_packets, step, (uint64_t)dir, seed, thr, owner, reliable, arrived);
+    return hipGetLastError();
+}
+
+__global__ __launch_bounds__(kThreads) void k_ages_update(int64_t total, const uint8_t* arrived,
+                                                          uint16_t* ages) {
+    for (int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x; idx < total;
+         idx += (int64_t)gridDim.x * kThreads) {
+        const uint16_t a = ages[idx];
+        ages[idx] = arrived[idx] ? 0 : (a == 0xFFFF ? 0xFFFF : a + 1);
+    }
+}
+
+hipError_t launch_ages_update(int64_t total, const uint8_t* arrived, uint16_t* ages,
+                              hipStream_t s) {
+    const int64_t blocks = grid_cap((total + kThreads - 1) / kThreads);
+    hipLaunchKernelGGL(k_ages_update, dim3((unsigned)blocks), dim3(kThreads), 0, s, total, arrived,
+                       ages);
     return hipGetLastError();
 }
 

@@ -201,7 +201,16 @@ struct MaskSource {
     bool draw;
     uint64_t seed, thr;
     const uint8_t* mem;
+    // Transfers that cannot be lost: row `owner` (-1 none) and packets with
+    // reliable[k] = 1 (reliable may be null) always arrive.
+    int owner;
+    const uint8_t* reliable;
 };
+
+__device__ __forceinline__ bool forced_arrival(int i, int64_t k, int owner,
+                                               const uint8_t* reliable) {
+    return i == owner || (reliable != nullptr && reliable[k] != 0);
+}
 
 // Stage the masks of packet k for `ndir` directions into words[dir][w].
 // All NT threads of the workgroup must call it (it ends with a barrier).
@@ -222,6 +231,7 @@ __device__ __forceinline__ void stage_masks(int ndir, const MaskSource* src, int
                                             src[s].seed, src[s].thr);
             else
                 arrived = src[s].mem[(int64_t)i * num_packets + k] != 0;
+            arrived = arrived || forced_arrival(i, k, src[s].owner, src[s].reliable);
         }
         const uint64_t word = __ballot(arrived);
         if ((threadIdx.x & 63) == 0) words[s][i >> 6] = word;
@@ -236,18 +246,68 @@ __device__ __forceinline__ int popcount_words(const uint64_t* words, int nw) {
 }
 
 // ---------------------------------------------------------------------------
-// Aggregate (Section 3 step (2)): g[j] = sum over arrived rows, ascending, of
-// grads[i][e0 + j], divided by K; lam * theta when K = 0.
+// Aggregate of one packet's contributions, 8 elements per thread.
 // ---------------------------------------------------------------------------
+enum { kEstArrivedMean = 0, kEstHorvitzThompson = 1, kEstStaleFill = 2 };
+
+struct AggVariant {
+    int kind;                 // kEst*
+    int owner;                // row that cannot be lost, or -1
+    float invq;               // 1 / arrival probability (Horvitz-Thompson)
+    const uint8_t* reliable;  // [P] packets that cannot be lost, or null
+    void* g_prev;             // [n][ld] last arrived contributions (stale fill)
+};
+
+// Arrived mean (Section 3 step (2)): g = (sum over arrived rows, ascending, in
+// fp32) / K, or lam * theta when K = 0.
+// Horvitz-Thompson: g = (sum over arrived lossy rows * (1/q) + the owner's row)
+// / n; on a reliable packet every row has weight 1, g = sum / n.
+// Stale fill (Algorithm 1): every row in ascending order contributes its
+// arrived value or, if lost, its last arrived one from g_prev; arrived values
+// are written to g_prev; g = sum / n.
 template <class E>
 __device__ __forceinline__ void aggregate8(const typename E::T* grads, int64_t ld,
                                            int64_t e0, int nv, const uint64_t* gm, int nw,
-                                           int K, float lam, const float (&th)[8],
+                                           int n, int K, float lam, const float (&th)[8],
+                                           const AggVariant& var, bool reliable_packet,
                                            float (&g)[8]) {
 #pragma unroll
     for (int j = 0; j < 8; ++j) g[j] = 0.0f;
+    if (var.kind == kEstStaleFill) {
+        typename E::T* prev = reinterpret_cast<typename E::T*>(var.g_prev);
+        for (int i0 = 0; i0 < n; i0 += kBatchGrad) {
+            float x[kBatchGrad][8];
+            bool arr[kBatchGrad];
+#pragma unroll
+            for (int u = 0; u < kBatchGrad; ++u) {
+                const int row = i0 + u < n ? i0 + u : i0;
+                arr[u] = (uniform64(gm[row >> 6]) >> (row & 63)) & 1;
+                const typename E::T* src = arr[u] ? grads : prev;
+                load8<E>(src + (int64_t)row * ld + e0, nv, x[u]);
+            }
+#pragma unroll
+            for (int u = 0; u < kBatchGrad; ++u) {
+                if (i0 + u < n) {
+#pragma unroll
+                    for (int j = 0; j < 8; ++j) g[j] += x[u][j];
+                    if (arr[u]) {
+                        Packed8<E> keep;
+                        keep.pack(x[u]);
+                        keep.store(prev + (int64_t)(i0 + u) * ld + e0, nv);
+                    }
+                }
+            }
+        }
+        const float nf = (float)n;
+#pragma unroll
+        for (int j = 0; j < 8; ++j) g[j] = g[j] / nf;
+        return;
+    }
+    const bool ht = var.kind == kEstHorvitzThompson;
+    const int sure_row = (ht && !reliable_packet) ? var.owner : -1;
     for (int w = 0; w < nw; ++w) {
         uint64_t bits = uniform64(gm[w]);
+        if (sure_row >= 0 && (sure_row >> 6) == w) bits &= ~(1ull << (sure_row & 63));
         while (bits) {
             int idx[kBatchGrad];
 #pragma unroll
@@ -270,7 +330,18 @@ __device__ __forceinline__ void aggregate8(const typename E::T* grads, int64_t l
             }
         }
     }
-    if (K > 0) {
+    if (ht) {
+        const float nf = (float)n;
+        if (reliable_packet) {
+#pragma unroll
+            for (int j = 0; j < 8; ++j) g[j] = g[j] / nf;
+        } else {
+            float own[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+            if (sure_row >= 0) load8<E>(grads + (int64_t)sure_row * ld + e0, nv, own);
+#pragma unroll
+            for (int j = 0; j < 8; ++j) g[j] = (g[j] * var.invq + own[j]) / nf;
+        }
+    } else if (K > 0) {
         const float kf = (float)K;
 #pragma unroll
         for (int j = 0; j < 8; ++j) g[j] = g[j] / kf;

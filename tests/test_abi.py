@@ -22,7 +22,7 @@ def test_header_declares_the_boundary():
     names = set(_declared())
     assert names == {"ll_masks", "lossy_aggregate", "shard_step", "lossy_broadcast",
                      "drift_stats", "lossy_step_fused", "ll_workspace_bytes",
-                     "ll_masks_workspace_bytes", "ll_last_error"}
+                     "ll_masks_workspace_bytes", "ll_ages_update", "ll_last_error"}
 
 
 def test_library_exports_every_declared_symbol():
@@ -38,6 +38,7 @@ def test_library_exports_every_declared_symbol():
 def test_struct_layouts():
     assert ctypes.sizeof(ll.LossSpec) == 56
     assert ctypes.sizeof(ll.OptSpec) == 28
+    assert ctypes.sizeof(ll.Ext) == 40
 
 
 def test_workspace_bytes_host_logic():
@@ -85,8 +86,8 @@ def test_aggregate_rejects_bad_arguments(args, code, frag):
     f = lib.lossy_aggregate
     f.argtypes = [ctypes.c_int32, ctypes.c_int64, ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p,
                   ctypes.c_int64, ctypes.c_void_p, ctypes.c_float, ctypes.c_void_p,
-                  ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
-    assert f(*args) == code
+                  ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+    assert f(*args[:11], None, args[11]) == code
     lib.ll_last_error.restype = ctypes.c_char_p
     assert frag in lib.ll_last_error().decode()
 
@@ -98,17 +99,17 @@ def test_masks_and_opt_validation():
     fm = lib.ll_masks
     fm.argtypes = [ctypes.c_int32, ctypes.c_int64, ctypes.c_uint64, ctypes.c_int32,
                    ctypes.POINTER(ll.LossSpec), ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
-                   ctypes.c_size_t, ctypes.c_void_p]
-    assert fm(4, 10, 0, 0, ctypes.byref(bad_p), None, 16, None, 0, None) == -1
+                   ctypes.c_size_t, ctypes.c_void_p, ctypes.c_void_p]
+    assert fm(4, 10, 0, 0, ctypes.byref(bad_p), None, 16, None, 0, None, None) == -1
     assert "p outside" in lib.ll_last_error().decode()
     ge = ll.gilbert_elliott(0.1, 0.2, 0.0, 0.5)
-    assert fm(4, 10, 0, 0, ctypes.byref(ge), None, 16, None, 0, None) == -1
+    assert fm(4, 10, 0, 0, ctypes.byref(ge), None, 16, None, 0, None, None) == -1
     assert "ge_state" in lib.ll_last_error().decode()
-    assert fm(4, 10, 0, 0, ctypes.byref(ge), 16, 16, None, 0, None) == -1
+    assert fm(4, 10, 0, 0, ctypes.byref(ge), 16, 16, None, 0, None, None) == -1
     assert "workspace" in lib.ll_last_error().decode()
-    assert fm(4, 10, 0, 3, ctypes.byref(ll.bernoulli(0.1)), None, 16, None, 0, None) == -1
+    assert fm(4, 10, 0, 3, ctypes.byref(ll.bernoulli(0.1)), None, 16, None, 0, None, None) == -1
     # Zero packets is a valid no-op that touches no device.
-    assert fm(4, 0, 0, 0, ctypes.byref(ll.bernoulli(0.1)), None, 16, None, 0, None) == 0
+    assert fm(4, 0, 0, 0, ctypes.byref(ll.bernoulli(0.1)), None, 16, None, 0, None, None) == 0
 
     fs = lib.shard_step
     fs.argtypes = [ctypes.POINTER(ll.OptSpec), ctypes.c_int64, ctypes.c_uint64, ctypes.c_void_p,
@@ -123,3 +124,26 @@ def test_masks_and_opt_validation():
     assert "unknown optimizer" in lib.ll_last_error().decode()
     # d = 0 returns before touching the device.
     assert fs(ctypes.byref(ll.sgd(0.1)), 0, 0, 16, None, None, 16, None) == 0
+
+
+def test_ext_validation():
+    lib = _raw()
+    lib.ll_last_error.restype = ctypes.c_char_p
+    f = lib.lossy_aggregate
+    f.argtypes = [ctypes.c_int32, ctypes.c_int64, ctypes.c_int64, ctypes.c_int32, ctypes.c_void_p,
+                  ctypes.c_int64, ctypes.c_void_p, ctypes.c_float, ctypes.c_void_p,
+                  ctypes.c_void_p, ctypes.c_void_p, ctypes.POINTER(ll.Ext), ctypes.c_void_p]
+    base = (4, 16, 8, 0, 16, 16, 16, 0.0, None, 16, None)
+    cases = [(ll.Ext(7, -1, None, None, None, 0.0), "unknown estimator"),
+             (ll.Ext(0, 4, None, None, None, 0.0), "owner=4"),
+             (ll.Ext(0, -2, None, None, None, 0.0), "owner=-2"),
+             (ll.Ext(1, -1, None, None, None, 0.0), "arrival probability"),
+             (ll.Ext(1, -1, None, None, None, 1.5), "arrival_prob"),
+             (ll.Ext(2, -1, None, None, None, 0.0), "g_prev is NULL")]
+    for e, frag in cases:
+        assert f(*base, ctypes.byref(e), None) == -1
+        assert frag in lib.ll_last_error().decode(), (frag, lib.ll_last_error())
+    fa = lib.ll_ages_update
+    fa.argtypes = [ctypes.c_int32, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
+    assert fa(4, 10, None, 16, None) == -1
+    assert fa(4, 0, None, None, None) == 0

@@ -53,7 +53,7 @@ class DeviceState:
                                      dtype=torch.uint8, device=device)
         self.drift = ll.drift_buffer(device)
 
-    def fused(self, step: int, drift=True, lam: float = 0.0, masks_out=True):
+    def fused(self, step: int, drift=True, lam: float = 0.0, masks_out=True, ext=None):
         w = self.w
         spec = loss_spec(w)
         ll.lossy_step_fused(
@@ -63,4 +63,4 @@ class DeviceState:
             arrived_g=self.arrived_g if masks_out else None,
             arrived_b=self.arrived_b if masks_out else None,
             counts=self.counts if masks_out else None, workspace=self.workspace,
-            drift=self.drift if drift else None)
+            drift=self.drift if drift else None, ext=ext)
