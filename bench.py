@@ -47,8 +47,12 @@ def kernel_source_hash() -> str:
     return h.hexdigest()[:16]
 
 
-def algorithmic_bytes(w, mg, mb, lens, drift: bool) -> dict:
-    """Bytes the step must move given realised masks (numpy [n][P] arrays)."""
+def algorithmic_bytes(w, mg, mb, lens, drift: bool, estimator: str = "arrived_mean",
+                      ages: bool = False, reliable: bool = False) -> dict:
+    """Bytes the step must move given realised masks (numpy [n][P] arrays).
+    The stale-fill estimator also reads the last arrived value of every lost
+    contribution and stores every arrived one; ages are read and written
+    once per (replica, packet); reliable flags are read once per packet."""
     import numpy as np
     eb = w.elem_bytes
     K = mg.sum(axis=0).astype(np.int64)
@@ -62,6 +66,13 @@ def algorithmic_bytes(w, mg, mb, lens, drift: bool) -> dict:
         replicas_written=int((R * lens).sum()) * eb,
         stale_read=int(((w.n - R) * lens).sum()) * eb if drift else 0,
     )
+    if estimator == "stale_fill":
+        out["g_prev_read"] = int(((w.n - K) * lens).sum()) * eb
+        out["g_prev_written"] = int((K * lens).sum()) * eb
+    if ages:
+        out["ages_rw"] = 2 * 2 * w.n * len(lens)
+    if reliable:
+        out["reliable_read"] = len(lens)
     out["total"] = sum(out.values())
     return out
 
@@ -172,7 +183,16 @@ def main():
     ap.add_argument("--cpu-packets", type=int, default=768,
                     help="packets of the workload the CPU oracle baseline runs on")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--estimator", default="arrived_mean",
+                    choices=["arrived_mean", "horvitz_thompson", "stale_fill"])
+    ap.add_argument("--owner", type=int, default=-1,
+                    help="row whose gradient and replica never cross the network")
+    ap.add_argument("--reliable-every", type=int, default=0,
+                    help="flag every k-th packet as sent over a reliable channel")
+    ap.add_argument("--ages", action="store_true", help="track broadcast ages")
     args = ap.parse_args()
+    variant = (args.estimator != "arrived_mean" or args.owner >= 0 or args.reliable_every > 0
+               or args.ages)
 
     if args.gpus != 1:
         print(f"bench.py measures one GPU only: this build simulates the N workers of one "
@@ -196,10 +216,27 @@ def main():
     log(f"plain 2 GiB device copy: {copy_gbs:.0f} GB/s")
     log(f"workload {name}: n={w.n} d={w.d} packet={w.packet} P={w.num_packets}")
     dev = DeviceState(w)
+    ext = None
+    rel_np = None
+    if variant:
+        rel_t = None
+        if args.reliable_every > 0:
+            rel_np = np.zeros(w.num_packets, np.uint8)
+            rel_np[:: args.reliable_every] = 1
+            rel_t = torch.from_numpy(rel_np).cuda()
+        q = 0.0
+        if args.estimator == "horvitz_thompson" and w.loss["kind"] != wl.BERNOULLI:
+            l = w.loss
+            pi_bad = l["p_gb"] / (l["p_gb"] + l["p_bg"])
+            q = 1 - pi_bad * l["loss_bad"] - (1 - pi_bad) * l["loss_good"]
+        ext = ll.ext(estimator=args.estimator, owner=args.owner, reliable=rel_t,
+                     g_prev=torch.zeros_like(dev.grads) if args.estimator == "stale_fill" else None,
+                     ages=(torch.zeros((w.n, w.num_packets), dtype=torch.int16, device="cuda")
+                           if args.ages else None), arrival_prob=q)
     torch.cuda.synchronize()
 
     cpu = None
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and not variant:
         log(f"timing the CPU oracle on {args.cpu_packets} packets ...")
         cpu = cpu_baseline(w, dev, args.cpu_packets)
         log(f"cpu oracle: {cpu}")
@@ -215,15 +252,19 @@ def main():
     ge_ws = torch.zeros(max(ll.ll_masks_workspace_bytes(w.n, P), 256), dtype=torch.uint8,
                         device="cuda")
     per_step_bytes = []
+    mext = None if ext is None else ll.ext(owner=args.owner, reliable=ext._tensors[0])
     for t in range(args.warmup + args.steps):
-        ll.ll_masks(w.n, P, t, ll.LL_DIR_GRAD, spec, mg_dev, ge_state=ge_g, workspace=ge_ws)
-        ll.ll_masks(w.n, P, t, ll.LL_DIR_BCAST, spec, mb_dev, ge_state=ge_b, workspace=ge_ws)
+        ll.ll_masks(w.n, P, t, ll.LL_DIR_GRAD, spec, mg_dev, ge_state=ge_g, workspace=ge_ws,
+                    ext=mext)
+        ll.ll_masks(w.n, P, t, ll.LL_DIR_BCAST, spec, mb_dev, ge_state=ge_b, workspace=ge_ws,
+                    ext=mext)
         if t >= args.warmup:
-            per_step_bytes.append(algorithmic_bytes(w, mg_dev.cpu().numpy(),
-                                                    mb_dev.cpu().numpy(), lens, True))
+            per_step_bytes.append(algorithmic_bytes(
+                w, mg_dev.cpu().numpy(), mb_dev.cpu().numpy(), lens, True,
+                estimator=args.estimator, ages=args.ages, reliable=rel_np is not None))
 
     for t in range(args.warmup):
-        dev.fused(t, masks_out=False)
+        dev.fused(t, masks_out=False, ext=ext)
     torch.cuda.synchronize()
 
     stream = torch.cuda.current_stream()
@@ -233,7 +274,7 @@ def main():
     wall0 = time.perf_counter()
     for j in range(args.steps):
         starts[j].record(stream)
-        dev.fused(args.warmup + j, masks_out=False)
+        dev.fused(args.warmup + j, masks_out=False, ext=ext)
         ends[j].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
@@ -268,7 +309,9 @@ def main():
         "config": {"workload": name, "n": w.n, "d": w.d, "packet": w.packet,
                    "packets": P, "loss": w.loss, "optimizer": w.opt["kind"],
                    "grad_dtype": w.gdtype, "replica_dtype": w.gdtype,
-                   "drift": True, "parallelism": "single-gpu simulation of n workers"},
+                   "drift": True, "parallelism": "single-gpu simulation of n workers",
+                   "estimator": args.estimator, "owner": args.owner,
+                   "reliable_every": args.reliable_every, "ages": args.ages},
         "pct_hbm_peak": round(100.0 * value / HBM_PEAK_GBS, 2),
         "elements_per_s": round(w.n * w.d / (ms_per_step * 1e-3), 1),
         "shard_elements_per_s": round(w.d / (ms_per_step * 1e-3), 1),
