@@ -19,6 +19,13 @@ Markov chain over the packet sequence (step-major, then packet), starting in
 Good before step 0.  Per packet the state first moves (Good->Bad when
 hi32(w0) < ceil(p_gb 2^32), Bad->Good when hi32(w0) < ceil(p_bg 2^32)), then
 the packet is lost when hi32(w1) < ceil(loss_state 2^32).
+
+Parity packets (erasure coding, proposed in Section 5 for shards whose loss
+hurts most): per row and group of G consecutive packets, one XOR parity
+packet travels under the same Bernoulli p, drawn with counter (group, i, t,
+dir + 2).  A group that lost exactly one packet, with its parity packet
+arrived, rebuilds that packet bit for bit, so recovery changes only the
+arrival indicators.
 """
 from __future__ import annotations
 
@@ -100,3 +107,38 @@ def apply_overrides(arrived: np.ndarray, owner: int = -1, reliable=None) -> np.n
     if reliable is not None:
         out[:, np.asarray(reliable).astype(bool)] = 1
     return out
+
+
+def parity_arrivals(seed: int, t: int, direction: int, n: int, groups, p: float):
+    """Arrival of each worker's parity packet for the given packet groups:
+    the same Bernoulli rule, drawn on direction dir + 2 (2 = gradient
+    parity, 3 = broadcast parity) with the group index in the packet slot."""
+    return bernoulli_arrivals(seed, t, direction + 2, n, groups, p)
+
+
+def parity_recover(arrived: np.ndarray, group: int, parity_arrived: np.ndarray) -> np.ndarray:
+    """Erasure coding over groups of `group` consecutive packets (the parity
+    packets the paper's Section 5 proposes): a worker that sends an XOR
+    parity packet per group lets the receiver rebuild exactly one lost packet
+    of that group, bit for bit, when the parity packet itself arrived.
+
+    arrived: uint8 [n][P] (after overrides); parity_arrived: uint8
+    [n][ceil(P / group)].  Returns the arrivals after recovery.
+    """
+    n, P = arrived.shape
+    out = np.array(arrived, dtype=np.uint8, copy=True)
+    for gi in range((P + group - 1) // group):
+        lo, hi = gi * group, min((gi + 1) * group, P)
+        for i in range(n):
+            lost = [k for k in range(lo, hi) if out[i, k] == 0]
+            if len(lost) == 1 and parity_arrived[i, gi]:
+                out[i, lost[0]] = 1
+    return out
+
+
+def parity_arrival_probability(q: float, group: int) -> float:
+    """Marginal arrival probability of a packet in a full group of `group`
+    i.i.d. packets plus parity, each arriving with probability q: it arrives,
+    or it alone was lost and the other group - 1 packets and the parity
+    packet arrived."""
+    return q + (1.0 - q) * q**group

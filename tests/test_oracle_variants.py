@@ -166,3 +166,76 @@ def test_replicas_are_the_master_of_their_age_and_drift_matches_ages(owner):
     assert abs(np.mean(ratio_pairs) - 1) < 0.05
     if owner >= 0:
         assert abs(np.mean(ratio_owner) - p / (1 - p)) < 0.05 * p / (1 - p)
+
+
+def test_parity_recovery_worked_example():
+    a = np.array([[1, 0, 1, 1, 0, 0, 1],
+                  [0, 1, 1, 1, 1, 1, 0]], np.uint8)
+    par = np.array([[1, 1], [0, 1]], np.uint8)  # group 4: packets 0-3, 4-6
+    out = loss.parity_recover(a, 4, par)
+    # row 0: group 0 lost one (k=1) and parity arrived -> rebuilt; group 1
+    # lost two -> nothing.  row 1: group 0 parity lost -> nothing; group 1
+    # lost one (k=6) and parity arrived -> rebuilt.
+    assert out.tolist() == [[1, 1, 1, 1, 0, 0, 1], [0, 1, 1, 1, 1, 1, 1]]
+
+
+@pytest.mark.parametrize("group,p", [(4, 0.1), (8, 0.2), (3, 0.4)])
+def test_parity_residual_loss_rate(group, p):
+    # A packet stays lost iff it was lost and not (every other packet of its
+    # group and the parity packet arrived): rate p (1 - (1 - p)^group).
+    n, P = 64, 4096 - 4096 % group
+    a = loss.bernoulli_arrivals(1, 0, loss.GRAD, n, np.arange(P), p)
+    par = loss.parity_arrivals(1, 0, loss.GRAD, n, np.arange(P // group), p)
+    out = loss.parity_recover(a, group, par)
+    q = 1 - loss.threshold(p) / 2**32
+    want = (1 - q) * (1 - q**group)
+    lost = out.size - int(out.sum())
+    sigma = np.sqrt(out.size * want * (1 - want) * 2)  # packets of a group are dependent
+    assert abs(lost - out.size * want) < 5 * sigma, (lost / out.size, want)
+    assert (out >= a).all()  # recovery only adds arrivals
+
+
+def test_parity_enumeration_single_group():
+    # Exact: over all loss patterns of one group plus its parity packet, the
+    # expected number of packets still lost is G p (1 - q^G).
+    G, p = 3, 0.3
+    q = 1 - p
+    expect = 0.0
+    for bits in itertools.product((0, 1), repeat=G + 1):
+        s = np.array(bits[:G], np.uint8)[None, :]
+        par = np.array([[bits[G]]], np.uint8)
+        pr = np.prod([q if b else p for b in bits])
+        out = loss.parity_recover(s, G, par)
+        expect += pr * (G - int(out.sum()))
+    assert abs(expect - G * p * (1 - q**G)) < 1e-12
+
+
+@pytest.mark.parametrize("G,q", [(1, 0.5), (3, 0.7), (5, 0.9)])
+def test_parity_marginal_arrival_by_enumeration(G, q):
+    # Every packet's marginal arrival probability over all 2^(G+1) patterns.
+    marg = np.zeros(G)
+    for bits in itertools.product((0, 1), repeat=G + 1):
+        pr = np.prod([q if b else 1 - q for b in bits])
+        out = loss.parity_recover(np.array(bits[:G], np.uint8)[None, :], G,
+                                  np.array([[bits[G]]], np.uint8))
+        marg += pr * out[0]
+    assert np.allclose(marg, loss.parity_arrival_probability(q, G), atol=1e-14)
+    # G = 1 is a duplicate send: lost only if both copies are lost.
+    if G == 1:
+        assert abs(marg[0] - (1 - (1 - q) ** 2)) < 1e-14
+
+
+def test_parity_respects_overrides_and_ragged_tail():
+    # Reliable packets count as present inside a group; the owner row never
+    # needs recovery; the last group of 7 packets under G = 3 holds one.
+    a = np.array([[0, 1, 1, 0, 0, 1, 0],
+                  [0, 0, 0, 0, 0, 0, 0]], np.uint8)
+    rel = np.array([0, 0, 0, 0, 1, 0, 0], np.uint8)
+    s = loss.apply_overrides(a, owner=1, reliable=rel)
+    par = np.ones((2, 3), np.uint8)
+    out = loss.parity_recover(s, 3, par)
+    # row 0: group 0 (k 0-2) one lost -> rebuilt; group 1 (k 3-5) k=4 is
+    # reliable, one lost (k=3) -> rebuilt; group 2 (k=6) lost -> rebuilt.
+    assert out.tolist() == [[1] * 7, [1] * 7]
+    par[0, 2] = 0
+    assert loss.parity_recover(s, 3, par)[0, 6] == 0
