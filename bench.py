@@ -190,9 +190,11 @@ def main():
     ap.add_argument("--reliable-every", type=int, default=0,
                     help="flag every k-th packet as sent over a reliable channel")
     ap.add_argument("--ages", action="store_true", help="track broadcast ages")
+    ap.add_argument("--parity-group", type=int, default=0,
+                    help="packets per XOR parity packet (0: no parity packets)")
     args = ap.parse_args()
     variant = (args.estimator != "arrived_mean" or args.owner >= 0 or args.reliable_every > 0
-               or args.ages)
+               or args.ages or args.parity_group > 0)
 
     if args.gpus != 1:
         print(f"bench.py measures one GPU only: this build simulates the N workers of one "
@@ -232,7 +234,8 @@ def main():
         ext = ll.ext(estimator=args.estimator, owner=args.owner, reliable=rel_t,
                      g_prev=torch.zeros_like(dev.grads) if args.estimator == "stale_fill" else None,
                      ages=(torch.zeros((w.n, w.num_packets), dtype=torch.int16, device="cuda")
-                           if args.ages else None), arrival_prob=q)
+                           if args.ages else None), arrival_prob=q,
+                     parity_group=args.parity_group)
     torch.cuda.synchronize()
 
     cpu = None
@@ -252,7 +255,8 @@ def main():
     ge_ws = torch.zeros(max(ll.ll_masks_workspace_bytes(w.n, P), 256), dtype=torch.uint8,
                         device="cuda")
     per_step_bytes = []
-    mext = None if ext is None else ll.ext(owner=args.owner, reliable=ext._tensors[0])
+    mext = None if ext is None else ll.ext(owner=args.owner, reliable=ext._tensors[0],
+                                           parity_group=args.parity_group)
     for t in range(args.warmup + args.steps):
         ll.ll_masks(w.n, P, t, ll.LL_DIR_GRAD, spec, mg_dev, ge_state=ge_g, workspace=ge_ws,
                     ext=mext)
@@ -311,7 +315,8 @@ def main():
                    "grad_dtype": w.gdtype, "replica_dtype": w.gdtype,
                    "drift": True, "parallelism": "single-gpu simulation of n workers",
                    "estimator": args.estimator, "owner": args.owner,
-                   "reliable_every": args.reliable_every, "ages": args.ages},
+                   "reliable_every": args.reliable_every, "ages": args.ages,
+                   "parity_group": args.parity_group},
         "pct_hbm_peak": round(100.0 * value / HBM_PEAK_GBS, 2),
         "elements_per_s": round(w.n * w.d / (ms_per_step * 1e-3), 1),
         "shard_elements_per_s": round(w.d / (ms_per_step * 1e-3), 1),

@@ -151,10 +151,24 @@ typedef struct {
  *                 steps since each replica packet last received the broadcast
  *                 (0 = this step; saturates at 65535).
  *   arrival_prob  q of LL_EST_HORVITZ_THOMPSON in (0, 1].  lossy_aggregate
- *                 requires it; lossy_step_fused takes 0 to mean 1 - p of a
- *                 Bernoulli gradient loss.
+ *                 requires it; lossy_step_fused takes 0 to mean the arrival
+ *                 probability of a Bernoulli gradient loss: 1 - p, or with
+ *                 parity packets q + (1 - q) q^G (q = 1 - p), which needs
+ *                 reliable == NULL and P a multiple of G.
+ *   parity_group  0 (none), or G in [1, 256]: erasure coding over groups of G
+ *                 consecutive packets (the parity packets proposed in the
+ *                 paper's Section 5).  Per row and group, the sender adds one
+ *                 XOR parity packet; when exactly one packet of the group was
+ *                 lost and the parity packet arrived, the receiver rebuilds
+ *                 the lost packet bit for bit, so it counts as arrived.  The
+ *                 last group of a row may be shorter.  The parity packet of
+ *                 group j in direction dir is lost under the same Bernoulli p,
+ *                 drawn with counter (j, i, t, dir + 2).  Bernoulli loss only
+ *                 (LL_EINVAL for Gilbert-Elliott).  G = 1 sends every packet
+ *                 twice.
  * Masks read from memory (lossy_aggregate, lossy_broadcast, drift_stats) are
- * taken as given: ll_masks and lossy_step_fused apply owner and reliable.
+ * taken as given: ll_masks and lossy_step_fused apply owner, reliable and
+ * parity recovery, in that order.
  */
 typedef struct {
     int32_t estimator;
@@ -163,6 +177,7 @@ typedef struct {
     void* g_prev;
     uint16_t* ages;
     double arrival_prob;
+    int32_t parity_group;
 } ll_ext;
 
 /*
@@ -177,7 +192,8 @@ typedef struct {
  *   workspace        Gilbert-Elliott only: device scratch of ws_bytes >=
  *                    ll_masks_workspace_bytes(n, num_packets); ignored (may be
  *                    NULL) for Bernoulli.
- *   ext              NULL, or variants: owner and reliable force arrivals.
+ *   ext              NULL, or variants: owner and reliable force arrivals;
+ *                    parity_group adds parity recovery (Bernoulli only).
  */
 LL_API int ll_masks(int32_t n, int64_t num_packets, uint64_t step, int32_t dir,
                     const ll_loss* loss, uint8_t* ge_state, uint8_t* arrived,

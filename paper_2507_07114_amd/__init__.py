@@ -64,17 +64,19 @@ class Ext(ctypes.Structure):
     which also keeps the tensors behind its device pointers alive."""
     _fields_ = [("estimator", ctypes.c_int32), ("owner", ctypes.c_int32),
                 ("reliable", ctypes.c_void_p), ("g_prev", ctypes.c_void_p),
-                ("ages", ctypes.c_void_p), ("arrival_prob", ctypes.c_double)]
+                ("ages", ctypes.c_void_p), ("arrival_prob", ctypes.c_double),
+                ("parity_group", ctypes.c_int32)]
 
 
 def ext(estimator: str = "arrived_mean", owner: int = -1,
         reliable: Optional[torch.Tensor] = None, g_prev: Optional[torch.Tensor] = None,
-        ages: Optional[torch.Tensor] = None, arrival_prob: float = 0.0) -> Ext:
+        ages: Optional[torch.Tensor] = None, arrival_prob: float = 0.0,
+        parity_group: int = 0) -> Ext:
     if estimator not in ESTIMATORS:
         raise ValueError(f"unknown estimator {estimator!r}")
     e = Ext(ESTIMATORS[estimator], owner, _flat(reliable, "reliable", torch.uint8),
             None if g_prev is None else _rows(g_prev, "g_prev")[0],
-            _flat(ages, "ages", torch.int16), arrival_prob)
+            _flat(ages, "ages", torch.int16), arrival_prob, parity_group)
     e._tensors = (reliable, g_prev, ages)  # the pointers above stay valid while e lives
     return e
 

@@ -184,6 +184,7 @@ struct ExtView {
     void* g_prev = nullptr;
     uint16_t* ages = nullptr;
     double q = 0.0;
+    int parity = 0;  // packets per parity group, 0 = no parity packets
 };
 
 int read_ext(const ll_ext* e, int32_t n, ExtView* v) {
@@ -194,13 +195,40 @@ int read_ext(const ll_ext* e, int32_t n, ExtView* v) {
     if (e->owner < -1 || e->owner >= n) return fail(LL_EINVAL, "owner=%d outside [-1, n)", e->owner);
     if (!(e->arrival_prob >= 0.0 && e->arrival_prob <= 1.0))
         return fail(LL_EINVAL, "arrival_prob outside [0, 1]");
+    if (e->parity_group < 0 || e->parity_group > kMaxParityGroup)
+        return fail(LL_EINVAL, "parity_group=%d outside [0, %d]", e->parity_group, kMaxParityGroup);
     v->est = e->estimator;
     v->owner = e->owner;
     v->reliable = e->reliable;
     v->g_prev = e->g_prev;
     v->ages = e->ages;
     v->q = e->arrival_prob;
+    v->parity = e->parity_group;
     return LL_OK;
+}
+
+// Parity-packet mask launch for up to two Bernoulli directions.
+int make_parity(const ExtView& x, int32_t n, int64_t P, uint64_t step, ParityLaunch* L) {
+    L->ndir = 0;
+    L->n = n;
+    L->G = x.parity;
+    L->P = P;
+    L->groups = (P + x.parity - 1) / x.parity;
+    L->step = step;
+    if ((2 * (int64_t)n * L->groups + kThreads - 1) / kThreads > 0x7FFFFFFFll)
+        return fail(LL_EINVAL, "too many workgroups");
+    return LL_OK;
+}
+
+void add_parity_job(ParityLaunch* L, const ll_loss* l, int dir, const ExtView& x,
+                    uint8_t* arrived) {
+    ParityJob& j = L->job[L->ndir++];
+    j.dir = (uint64_t)dir;
+    j.seed = l->seed;
+    j.thr = threshold(l->p);
+    j.owner = x.owner;
+    j.reliable = x.reliable;
+    j.arrived = arrived;
 }
 
 // Aggregation variant for the kernels; q is the Horvitz-Thompson arrival
@@ -264,6 +292,7 @@ int ll_masks(int32_t n, int64_t num_packets, uint64_t step, int32_t dir, const l
     if ((r = read_ext(ext, n, &x))) return r;
     if (!arrived) return fail(LL_EINVAL, "arrived is NULL");
     const bool ge = loss->kind == LL_LOSS_GILBERT_ELLIOTT;
+    if (ge && x.parity) return fail(LL_EINVAL, "parity packets need Bernoulli loss");
     if (ge && !ge_state) return fail(LL_EINVAL, "ge_state is NULL for a Gilbert-Elliott process");
     const GeScratch gs = ge_scratch(n, num_packets);
     if (ge && (!workspace || ws_bytes < gs.per_dir))
@@ -271,6 +300,12 @@ int ll_masks(int32_t n, int64_t num_packets, uint64_t step, int32_t dir, const l
     if (num_packets == 0) return ok();
     if ((int64_t)n * gs.S > 0x7FFFFFFFll) return fail(LL_EINVAL, "too many workgroups");
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+    if (x.parity) {
+        ParityLaunch PL;
+        if ((r = make_parity(x, n, num_packets, step, &PL))) return r;
+        add_parity_job(&PL, loss, dir, x, arrived);
+        return hip_check(launch_masks_parity(PL, s), "ll_masks");
+    }
     if (!ge)
         return hip_check(launch_masks_bernoulli(n, num_packets, step, dir, loss->seed,
                                                 threshold(loss->p), x.owner, x.reliable, arrived,
@@ -428,6 +463,7 @@ int lossy_step_fused(int32_t n, int64_t d, int64_t packet, uint64_t step, const 
     const bool ge_b = loss_b->kind == LL_LOSS_GILBERT_ELLIOTT;
     if (ge_g && !ge_state_g) return fail(LL_EINVAL, "ge_state_g is NULL for a Gilbert-Elliott process");
     if (ge_b && !ge_state_b) return fail(LL_EINVAL, "ge_state_b is NULL for a Gilbert-Elliott process");
+    if (x.parity && (ge_g || ge_b)) return fail(LL_EINVAL, "parity packets need Bernoulli loss");
     if (drift && (r = check_vec("drift", drift, true))) return r;
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     if (d == 0) {
@@ -445,11 +481,20 @@ int lossy_step_fused(int32_t n, int64_t d, int64_t packet, uint64_t step, const 
         if (loss_g->kind != LL_LOSS_BERNOULLI)
             return fail(LL_EINVAL, "Horvitz-Thompson under Gilbert-Elliott loss needs arrival_prob");
         q = 1.0 - loss_g->p;
+        if (x.parity) {
+            // A packet also arrives when it alone was lost in its group and
+            // the parity packet came through: q + (1 - q) q^G, the same for
+            // every packet only when all groups are full and none is reliable.
+            if (x.reliable || g.P % x.parity != 0)
+                return fail(LL_EINVAL, "Horvitz-Thompson with parity packets needs arrival_prob "
+                                       "unless P is a multiple of parity_group and reliable is NULL");
+            q = q + (1.0 - q) * std::pow(q, (double)x.parity);
+        }
     }
     AggVariant var;
     if ((r = make_variant(x, q, x.g_prev, &var))) return r;
     const WsLayout w = ws_layout(n, g);
-    const bool need_ws = drift || ge_g || ge_b;
+    const bool need_ws = drift || ge_g || ge_b || x.parity;
     if (need_ws) {
         if (!workspace || ws_bytes < w.total)
             return fail(LL_EINVAL, "workspace of %zu bytes is smaller than %zu", ws_bytes, w.total);
@@ -506,6 +551,19 @@ int lossy_step_fused(int32_t n, int64_t d, int64_t packet, uint64_t step, const 
             if (dir == 0) p.out_g = nullptr;  // already written by the scan
             else p.out_b = nullptr;
         }
+    }
+    if (x.parity) {
+        // Recovery needs a whole group's arrivals: masks go through memory.
+        ParityLaunch PL;
+        if ((r = make_parity(x, n, g.P, step, &PL))) return r;
+        for (int dir = 0; dir < 2; ++dir) {
+            uint8_t* dst = outs[dir] ? outs[dir] : ws + w.partials + dir * w.masks;
+            add_parity_job(&PL, losses[dir], dir, x, dst);
+            p.src[dir] = MaskSource{false, 0, 0, dst, -1, nullptr};
+        }
+        p.out_g = p.out_b = nullptr;
+        r = hip_check(launch_masks_parity(PL, s), "lossy_step_fused (parity masks)");
+        if (r) return r;
     }
     if (nge) {
         if ((int64_t)nge * n * w.gs.S > 0x7FFFFFFFll) return fail(LL_EINVAL, "too many workgroups");

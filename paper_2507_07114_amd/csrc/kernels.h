@@ -131,6 +131,25 @@ struct FusedParams {
     uint16_t* ages;    // [n][P] broadcast ages, or null
 };
 
+// Largest packet group of the parity-packet recovery.
+constexpr int kMaxParityGroup = 256;
+
+// One direction's Bernoulli masks with parity recovery.
+struct ParityJob {
+    uint64_t dir, seed, thr;
+    int owner;
+    const uint8_t* reliable;  // [P] or null
+    uint8_t* arrived;         // [n][P] out
+};
+
+struct ParityLaunch {
+    int ndir, n, G;
+    int64_t P, groups;  // groups = ceil(P / G) per row
+    uint64_t step;
+    ParityJob job[2];
+};
+
+hipError_t launch_masks_parity(const ParityLaunch& L, hipStream_t s);
 hipError_t launch_masks_bernoulli(int n, int64_t num_packets, uint64_t step, int dir,
                                   uint64_t seed, uint64_t thr, int owner,
                                   const uint8_t* reliable, uint8_t* arrived, hipStream_t s);

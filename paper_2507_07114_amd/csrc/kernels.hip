@@ -33,6 +33,39 @@ __global__ __launch_bounds__(kThreads) void k_masks_bernoulli(int n, int64_t num
     }
 }
 
+// Bernoulli masks with parity packets: one thread per (direction, row, group
+// of G packets).  It draws the group's arrivals, applies the transfers that
+// cannot be lost, and when exactly one packet is missing and the group's
+// parity packet (counter (group, row, step, dir + 2)) arrived, marks that
+// packet arrived: XOR of the parity with the other G - 1 packets rebuilds it
+// exactly.
+__global__ __launch_bounds__(kThreads) void k_masks_parity(ParityLaunch L) {
+    const int64_t per_dir = (int64_t)L.n * L.groups;
+    const int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+    if (idx >= L.ndir * per_dir) return;
+    const int s = idx >= per_dir ? 1 : 0;
+    const ParityJob& J = L.job[s];
+    const int64_t rem = idx - s * per_dir;
+    const int64_t i = rem / L.groups;
+    const int64_t j = rem - i * L.groups;
+    const int64_t k0 = j * L.G;
+    const int64_t k1 = k0 + L.G < L.P ? k0 + L.G : L.P;
+    uint8_t* row = J.arrived + i * L.P;
+    int64_t missing = 0, last = -1;
+    for (int64_t k = k0; k < k1; ++k) {
+        const bool a = bernoulli_arrived((uint64_t)k, (uint64_t)i, L.step, J.dir, J.seed, J.thr) ||
+                       forced_arrival((int)i, k, J.owner, J.reliable);
+        row[k] = a ? 1 : 0;
+        if (!a) {
+            ++missing;
+            last = k;
+        }
+    }
+    if (missing == 1 &&
+        bernoulli_arrived((uint64_t)j, (uint64_t)i, L.step, J.dir + 2, J.seed, J.thr))
+        row[last] = 1;
+}
+
 // Gilbert-Elliott masks.  A chain's per-packet transition is a map on
 // {Good, Bad}, encoded in two bits (bit 0 = image of Good, bit 1 = image of
 // Bad); maps compose associatively, so the chain state before any packet is
@@ -466,6 +499,13 @@ hipError_t launch_masks_bernoulli(int n, int64_t num_packets, uint64_t step, int
     const int64_t blocks = grid_cap((total + kThreads - 1) / kThreads);
     hipLaunchKernelGGL(k_masks_bernoulli, dim3((unsigned)blocks), dim3(kThreads), 0, s, n,
                        num_packets, step, (uint64_t)dir, seed, thr, owner, reliable, arrived);
+    return hipGetLastError();
+}
+
+hipError_t launch_masks_parity(const ParityLaunch& L, hipStream_t s) {
+    const int64_t total = (int64_t)L.ndir * L.n * L.groups;
+    const int64_t blocks = (total + kThreads - 1) / kThreads;
+    hipLaunchKernelGGL(k_masks_parity, dim3((unsigned)blocks), dim3(kThreads), 0, s, L);
     return hipGetLastError();
 }
 

@@ -38,7 +38,8 @@ def test_library_exports_every_declared_symbol():
 def test_struct_layouts():
     assert ctypes.sizeof(ll.LossSpec) == 56
     assert ctypes.sizeof(ll.OptSpec) == 28
-    assert ctypes.sizeof(ll.Ext) == 40
+    assert ctypes.sizeof(ll.Ext) == 48
+    assert ll.Ext.parity_group.offset == 40
 
 
 def test_workspace_bytes_host_logic():
@@ -139,7 +140,9 @@ def test_ext_validation():
              (ll.Ext(0, -2, None, None, None, 0.0), "owner=-2"),
              (ll.Ext(1, -1, None, None, None, 0.0), "arrival probability"),
              (ll.Ext(1, -1, None, None, None, 1.5), "arrival_prob"),
-             (ll.Ext(2, -1, None, None, None, 0.0), "g_prev is NULL")]
+             (ll.Ext(2, -1, None, None, None, 0.0), "g_prev is NULL"),
+             (ll.Ext(0, -1, None, None, None, 0.0, -1), "parity_group=-1"),
+             (ll.Ext(0, -1, None, None, None, 0.0, 257), "parity_group=257")]
     for e, frag in cases:
         assert f(*base, ctypes.byref(e), None) == -1
         assert frag in lib.ll_last_error().decode(), (frag, lib.ll_last_error())
@@ -147,3 +150,47 @@ def test_ext_validation():
     fa.argtypes = [ctypes.c_int32, ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]
     assert fa(4, 10, None, 16, None) == -1
     assert fa(4, 0, None, None, None) == 0
+
+
+def test_parity_validation():
+    lib = _raw()
+    lib.ll_last_error.restype = ctypes.c_char_p
+    fm = lib.ll_masks
+    fm.argtypes = [ctypes.c_int32, ctypes.c_int64, ctypes.c_uint64, ctypes.c_int32,
+                   ctypes.POINTER(ll.LossSpec), ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                   ctypes.c_size_t, ctypes.POINTER(ll.Ext), ctypes.c_void_p]
+    ge = ll.gilbert_elliott(0.1, 0.2, 0.0, 0.5)
+    e = ll.Ext(0, -1, None, None, None, 0.0, 4)
+    assert fm(4, 10, 0, 0, ctypes.byref(ge), 16, 16, 16, 1 << 20, ctypes.byref(e), None) == -1
+    assert "Bernoulli" in lib.ll_last_error().decode()
+    # Zero packets stays a no-op with parity on.
+    assert fm(4, 0, 0, 0, ctypes.byref(ll.bernoulli(0.1)), None, 16, None, 0,
+              ctypes.byref(e), None) == 0
+
+    ff = lib.lossy_step_fused
+    ff.argtypes = [ctypes.c_int32, ctypes.c_int64, ctypes.c_int64, ctypes.c_uint64,
+                   ctypes.POINTER(ll.LossSpec), ctypes.POINTER(ll.LossSpec), ctypes.c_void_p,
+                   ctypes.c_void_p, ctypes.c_int32, ctypes.c_void_p, ctypes.c_int64,
+                   ctypes.POINTER(ll.OptSpec), ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                   ctypes.c_int32, ctypes.c_void_p, ctypes.c_int64, ctypes.c_void_p,
+                   ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t,
+                   ctypes.c_void_p, ctypes.POINTER(ll.Ext), ctypes.c_void_p]
+    b = ll.bernoulli(0.2)
+    sgd = ll.sgd(0.1)
+
+    def call(e, lb=b, d=64, packet=8):
+        return ff(4, d, packet, 0, ctypes.byref(b), ctypes.byref(lb), 16, 16, 0, 16, d,
+                  ctypes.byref(sgd), 16, None, None, 0, 16, d, None, None, None, None, 0,
+                  None, ctypes.byref(e), None)
+
+    assert call(ll.Ext(0, -1, None, None, None, 0.0, 4), lb=ge) == -1
+    assert "Bernoulli" in lib.ll_last_error().decode()
+    # Horvitz-Thompson with derived q: P = 8 packets is not a multiple of 3,
+    # and reliable flags make the arrival probability differ per packet.
+    assert call(ll.Ext(1, -1, None, None, None, 0.0, 3)) == -1
+    assert "parity_group" in lib.ll_last_error().decode()
+    assert call(ll.Ext(1, -1, 16, None, None, 0.0, 4)) == -1
+    assert "reliable" in lib.ll_last_error().decode()
+    # Everything valid but no workspace: parity masks go through memory.
+    assert call(ll.Ext(1, -1, None, None, None, 0.0, 4)) == -1
+    assert "workspace" in lib.ll_last_error().decode()

@@ -243,3 +243,84 @@ def test_replicas_hold_the_master_of_their_age():
     never = a >= len(history) - 1  # not refreshed since the start: initial copy
     assert np.array_equal(reps[~never].view(np.uint32), want[~never].view(np.uint32))
     assert (a[2] == 0).all()  # the owner's own replica is always current
+
+
+def _parity_masks(seed, t, direction, n, P, p, G, owner=-1, relf=None):
+    a = oloss.apply_overrides(oloss.bernoulli_arrivals(seed, t, direction, n, np.arange(P), p),
+                              owner, relf)
+    par = oloss.parity_arrivals(seed, t, direction, n, np.arange((P + G - 1) // G), p)
+    return oloss.parity_recover(a, G, par)
+
+
+@pytest.mark.parametrize("G,n,P,owner,rel", [
+    (1, 5, 3000, -1, False), (3, 9, 5003, 2, True), (8, 64, 4096, -1, False),
+    (8, 65, 2001, 64, True), (256, 4, 1000, -1, False), (256, 3, 200, 0, False),
+])
+def test_parity_masks_bit_exact(G, n, P, owner, rel):
+    print(f"parity masks G={G} n={n} P={P} owner={owner} rel={rel}", flush=True)
+    relf = _reliable(P) if rel else None
+    e = ll.ext(owner=owner, reliable=None if relf is None else _u8(relf), parity_group=G)
+    out = torch.full((n, P), 7, dtype=torch.uint8, device=DEV)
+    for t, direction in ((0, 0), (1, 1), (4, 0)):
+        ll.ll_masks(n, P, t, direction, ll.bernoulli(0.3, seed=11), out, ext=e)
+        want = _parity_masks(11, t, direction, n, P, 0.3, G, owner, relf)
+        assert np.array_equal(out.cpu().numpy(), want), (t, direction)
+
+
+@pytest.mark.parametrize("est,G,owner,rel", [
+    ("arrived_mean", 4, -1, False), ("arrived_mean", 3, 1, True),
+    ("horvitz_thompson", 6, -1, False), ("stale_fill", 2, 0, False),
+])
+def test_fused_parity_with_oracle(est, G, owner, rel):
+    # 2048 * 60 + 24 elements in packets of 2048: 61 packets, the last ragged
+    # (a multiple of G only for G = 1, so Horvitz-Thompson runs on 60 packets).
+    d = 2048 * 60 + (0 if est == "horvitz_thompson" else 24)
+    w = wl.scaled(wl.WORKLOADS["n8_d16m_bf16_adam"], d=d, steps=3,
+                  loss=dict(kind=wl.BERNOULLI, p=0.3))
+    print(f"fused parity {est} G={G} owner={owner} rel={rel}", flush=True)
+    dev = parity.DeviceState(w, pad=8)
+    relf, relt, prev, ages = _variant_setup(w, est, owner, rel, dev)
+    e = ll.ext(estimator=est, owner=owner, reliable=relt, g_prev=prev, ages=ages, parity_group=G)
+    packets = list(range(w.num_packets))
+    so = parity.SampledOracle(w, packets, dev)
+    prev_o = np.zeros((w.n, w.d), np.uint16)
+    p = w.loss["p"]
+    q = np.full((w.n, w.num_packets), oloss.parity_arrival_probability(1 - p, G))
+    if owner >= 0:
+        q[owner] = 1.0
+    for t in range(w.steps):
+        if t > 0:
+            wl.draw_grads(w, t, device=DEV, ld=dev.ld, out=dev.grads)
+        g_host = parity.host_rows(dev.grads, so.idx, w.gdtype)
+        dev.fused(t, ext=e)
+        mg = _parity_masks(w.seed, t, 0, w.n, w.num_packets, p, G, owner, relf)
+        mb = _parity_masks(w.seed, t, 1, w.n, w.num_packets, p, G, owner, relf)
+        assert np.array_equal(dev.arrived_g.cpu().numpy(), mg)
+        assert np.array_equal(dev.arrived_b.cpu().numpy(), mb)
+        orc = ostep.lossy_step(d=w.d, packet=w.packet, packets=packets, gdtype=w.gdtype,
+                               grads=g_host, theta=so.theta, m=so.m, v=so.v,
+                               replicas=so.replicas, arrived_g=mg, arrived_b=mb, opt=w.opt, t=t,
+                               estimator=est, q=q, g_prev=prev_o)
+        so.prev_replicas = so.replicas
+        so.theta, so.m, so.v, so.replicas = orc["theta"], orc["m"], orc["v"], orc["replicas"]
+        parity.compare_step(w, t, dev, so, orc, mb, f"{est} parity step {t}")
+        if est == "stale_fill":
+            prev_o = orc["g_prev"]
+        so.upload(dev)
+
+
+def test_fused_parity_masks_in_workspace_match_masks_out():
+    # With no mask outputs the parity masks live in the workspace; the step's
+    # results are the same bytes.
+    w = wl.scaled(wl.WORKLOADS["n8_d16m_bf16_adam"], d=2048 * 33 + 40, steps=2,
+                  loss=dict(kind=wl.BERNOULLI, p=0.4))
+    a = parity.DeviceState(w)
+    b = parity.DeviceState(w)
+    for t in range(2):
+        wl.draw_grads(w, t, device=DEV, ld=a.ld, out=a.grads)
+        b.grads.copy_(a.grads)
+        a.fused(t, ext=ll.ext(parity_group=5))
+        b.fused(t, masks_out=False, ext=ll.ext(parity_group=5))
+        for k in ("theta", "m", "v", "replicas"):
+            assert torch.equal(getattr(a, k).view(torch.uint8), getattr(b, k).view(torch.uint8)), k
+        assert ll.read_drift(a.drift) == ll.read_drift(b.drift)

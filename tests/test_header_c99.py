@@ -17,7 +17,7 @@ C_SOURCE = r"""
 int main(void) {
     ll_loss loss = {LL_LOSS_BERNOULLI, 0.1, 0.0, 0.0, 0.0, 0.0, 0};
     ll_opt opt = {LL_ADAM, 3e-4f, 0.0f, 0.9f, 0.95f, 1e-8f, 0.0f};
-    ll_ext ext = {LL_EST_ARRIVED_MEAN, -1, NULL, NULL, NULL, 0.0};
+    ll_ext ext = {LL_EST_ARRIVED_MEAN, -1, NULL, NULL, NULL, 0.0, 0};
     ll_drift drift;
     (void)drift;
     int rc = 0;
