@@ -100,3 +100,46 @@ def test_long_run_drift_is_bounded():
     assert abs(ratio - corrected) < 0.03 * corrected
     half = len(ms) // 2
     assert abs(ms[:half].mean() - ms[half:].mean()) < 0.03 * ms.mean()  # no growth
+
+
+def test_drift_workload_all_steps_on_a_packet_slice():
+    # Every one of the 200 steps of the N=64 drift workload at full size on
+    # the GPU; the oracle follows a slice of four packets (restarted from the
+    # device's state each step, so fp32 rounding order cannot accumulate),
+    # and drift_stats on the slice's sub-view is compared with the oracle's
+    # drift of the same replicas.
+    from oracle import drift as odrift
+    from oracle import loss as oloss
+    w = wl.WORKLOADS["n64_d48m_f32_sgd_drift"]
+    assert w.loss["kind"] == wl.BERNOULLI and w.gdtype == wl.F32
+    packets = [0, 1, 2, 3]
+    e1 = len(packets) * w.packet
+    dev = parity.DeviceState(w)
+    so = parity.SampledOracle(w, packets, dev)
+    out = ll.drift_buffer()
+    try:
+        for t in range(w.steps):
+            if t > 0:
+                wl.draw_grads(w, t, device=DEV, ld=dev.ld, out=dev.grads)
+            g_host = parity.host_rows(dev.grads, so.idx, w.gdtype)
+            dev.fused(t)
+            mg = oloss.bernoulli_arrivals(w.seed, t, 0, w.n, packets, w.loss["p"])
+            mb = oloss.bernoulli_arrivals(w.seed, t, 1, w.n, packets, w.loss["p"])
+            assert np.array_equal(dev.arrived_g[:, packets].cpu().numpy(), mg), f"step {t}"
+            assert np.array_equal(dev.arrived_b[:, packets].cpu().numpy(), mb), f"step {t}"
+            orc = so.step(t, g_host, mg, mb)
+            parity.compare_step(w, t, dev, so, orc, mb, f"slice step {t}")
+            ll.drift_stats(dev.replicas[:, :e1], d=e1, packet=w.packet, workspace=dev.workspace,
+                           out=out, theta=dev.theta[:e1])
+            r = ll.read_drift(out)
+            x = parity.host_rows(dev.replicas, so.idx, w.gdtype).astype(np.float64)
+            ref = odrift.drift_stats(x, master=parity.host_vec(dev.theta, so.idx).astype(np.float64))
+            assert r["max_abs"] == ref["max_abs"], f"step {t} max_abs"
+            for k in ("mean_sq", "mean_abs_to_master"):
+                assert abs(r[k] - ref[k]) <= 1e-9 * abs(ref[k]) + 1e-300, (t, k, r[k], ref[k])
+            so.upload(dev)
+            if t % 50 == 0:
+                print(f"  step {t}: slice rms drift {r['rms']:.3e}", flush=True)
+    finally:
+        del dev
+        _free()
