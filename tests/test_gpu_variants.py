@@ -134,8 +134,19 @@ def _variant_setup(w, est, owner, rel, dev):
 @pytest.mark.parametrize("name", ["n8_d16m_bf16_adam", "n16_d256m_f32_ge_momentum"])
 @pytest.mark.parametrize("est,owner,rel", VARIANTS)
 def test_fused_variants_bit_identical_to_stagewise(name, est, owner, rel):
-    w = wl.scaled(wl.WORKLOADS[name], d=4096 * 40 + 1000)
-    print(f"fused vs stagewise {name} {est} owner={owner} rel={rel}", flush=True)
+    _fused_vs_stagewise(wl.WORKLOADS[name], est, owner, rel, 0)
+
+
+@pytest.mark.parametrize("est,owner,rel,G", [
+    ("arrived_mean", -1, False, 4), ("stale_fill", 1, True, 3), ("arrived_mean", 0, True, 1),
+])
+def test_fused_parity_bit_identical_to_stagewise(est, owner, rel, G):
+    _fused_vs_stagewise(wl.WORKLOADS["n8_d16m_bf16_adam"], est, owner, rel, G)
+
+
+def _fused_vs_stagewise(w0, est, owner, rel, G):
+    w = wl.scaled(w0, d=4096 * 40 + 1000)
+    print(f"fused vs stagewise {w0.name} {est} owner={owner} rel={rel} parity={G}", flush=True)
     a = parity.DeviceState(w)
     b = parity.DeviceState(w)
     _, rel_a, prev_a, ages_a = _variant_setup(w, est, owner, rel, a)
@@ -149,8 +160,9 @@ def test_fused_variants_bit_identical_to_stagewise(name, est, owner, rel):
     # the fused side derives q itself for Bernoulli loss; GE needs it given
     qa = q if l["kind"] != wl.BERNOULLI else 0.0
     ea = ll.ext(estimator=est, owner=owner, reliable=rel_a, g_prev=prev_a, ages=ages_a,
-                arrival_prob=qa)
-    eb = ll.ext(estimator=est, owner=owner, reliable=rel_b, g_prev=prev_b, arrival_prob=q)
+                arrival_prob=qa, parity_group=G)
+    eb = ll.ext(estimator=est, owner=owner, reliable=rel_b, g_prev=prev_b, arrival_prob=q,
+                parity_group=G)
     spec = parity.loss_spec(w)
     P = w.num_packets
     for t in range(3):
