@@ -36,6 +36,13 @@ def test_known_answer_vectors_scalar_and_vector():
         assert tuple(int(w[0]) for w in got) == want
 
 
+def test_known_answer_vectors_agree_with_numpy():
+    # The stored vectors are themselves checked against the third-party
+    # implementation, so the fixture cannot carry a transcription error.
+    for r in _kat_rows():
+        assert _numpy_block(r[0:4], r[4:6]) == tuple(r[6:10])
+
+
 def _numpy_block(ctr, key):
     """Block at `ctr` from numpy's independent Philox (pre-increment)."""
     c = ctr[0] | (ctr[1] << 64) | (ctr[2] << 128) | (ctr[3] << 192)
