@@ -349,6 +349,9 @@ def main():
         "elements_per_s": round(w.n * w.d / (ms_per_step * 1e-3), 1),
         "shard_elements_per_s": round(w.d / (ms_per_step * 1e-3), 1),
         "algorithmic_bytes_per_step": mean_b,
+        # every gradient row read and every replica row written, as a
+        # loss-oblivious pass would move them (context for the count above)
+        "dense_equivalent_bytes_per_step": 2 * w.n * w.d * w.elem_bytes + mean_b["state_rw"],
         "hbm_copy_probe_gbs": round(copy_gbs, 1),
         "roofline": {
             "bound": "hbm",
