@@ -89,6 +89,36 @@ def test_fused_is_bit_identical_to_stagewise(name):
         assert stale == int((sa["arrived_b"] == 0).sum())
 
 
+@pytest.mark.parametrize("name,rdtype", [("n8_d16m_bf16_adam", torch.float32),
+                                         ("n64_d48m_f32_sgd_drift", torch.bfloat16),
+                                         ("n16_d256m_f32_ge_momentum", torch.bfloat16)])
+def test_mixed_row_dtypes_fused_bit_identical_to_stagewise(name, rdtype):
+    # Gradient and replica rows of different types (the other two of the four
+    # type pairs the library compiles): the fused step against the chain of
+    # one-stage calls, each of which is compared with the oracle per type.
+    w = _small(name)
+    print(f"mixed dtypes {name}: grads {w.gdtype}, replicas {rdtype}", flush=True)
+    a = parity.DeviceState(w)
+    b = parity.DeviceState(w)
+    for dev in (a, b):
+        dev.replicas = torch.zeros((w.n, dev.ld), dtype=rdtype, device=DEV)
+        dev.replicas[:, : w.d] = dev.theta.to(rdtype)[None, :]
+    for t in range(2):
+        wl.draw_grads(w, t, device=DEV, ld=a.ld, out=a.grads)
+        b.grads.copy_(a.grads)
+        a.fused(t)
+        _stagewise(b, t)
+        sa, sb = _snapshot(a), _snapshot(b)
+        sa["drift"]["empty_packets"] = sb["drift"]["empty_packets"] = 0
+        assert sa["drift"] == sb["drift"], (sa["drift"], sb["drift"])
+        for k in sa:
+            if k != "drift":
+                assert _bit_equal(sa[k], sb[k]), f"{name} step {t}: {k} differs"
+        R = a.arrived_b.repeat_interleave(w.packet, dim=1)[:, : w.d].bool()
+        own = a.theta.to(rdtype)[None, :].expand(w.n, -1)
+        assert _bit_equal(a.replicas[:, : w.d][R], own[R]), "arrived replica != rounded master"
+
+
 @pytest.mark.parametrize("name", list(SMALL))
 def test_fused_parity_with_oracle(name):
     w = _small(name)
