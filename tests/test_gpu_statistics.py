@@ -1,0 +1,106 @@
+"""Statistical properties of the GPU path over many seeded steps, and a
+worker that is lost for good.
+
+Monte Carlo: with fixed gradients, the GPU aggregate averaged over 20,000
+steps of Bernoulli masks (each step draws fresh masks from the counter-based
+generator) must match its exact expectation within 5.5 standard errors per
+element; the expectation and variance come from enumerating all 2^N masks
+(the arrived-mean estimator is unbiased given K > 0, so unconditionally
+E = (1 - p^N) mean with the zero fallback; Horvitz-Thompson is unbiased
+with no conditioning)."""
+import itertools
+
+import numpy as np
+import pytest
+import torch
+
+import paper_2507_07114_amd as ll
+
+pytestmark = pytest.mark.gpu
+DEV = "cuda"
+
+
+def _exact_moments(g: np.ndarray, p: float, estimator: str):
+    """Mean and variance per element over all 2^N arrival patterns of one packet."""
+    n = g.shape[0]
+    q = 1.0 - p
+    mean = np.zeros(g.shape[1])
+    second = np.zeros(g.shape[1])
+    for bits in itertools.product((0, 1), repeat=n):
+        s = np.array(bits, dtype=np.float64)
+        pr = float(np.prod(np.where(s == 1, q, p)))
+        k = s.sum()
+        if estimator == "arrived_mean":
+            gh = (s[:, None] * g).sum(axis=0) / k if k > 0 else np.zeros(g.shape[1])
+        else:
+            gh = (s[:, None] * g).sum(axis=0) / q / n
+        mean += pr * gh
+        second += pr * gh * gh
+    return mean, second - mean * mean
+
+
+@pytest.mark.parametrize("estimator", ["arrived_mean", "horvitz_thompson"])
+def test_monte_carlo_aggregate_matches_its_expectation(estimator):
+    n, L, P, p, T = 8, 256, 4, 0.3, 20_000
+    d = L * P
+    rng = np.random.default_rng(11)
+    g = rng.standard_normal((n, d)).astype(np.float32)
+    grads = torch.from_numpy(g).to(DEV)
+    masks = torch.empty((n, P), dtype=torch.uint8, device=DEV)
+    g_hat = torch.empty(d, dtype=torch.float32, device=DEV)
+    acc = torch.zeros(d, dtype=torch.float64, device=DEV)
+    e = ll.ext(estimator=estimator, arrival_prob=1 - p)
+    spec = ll.bernoulli(p, seed=3)
+    print(f"monte carlo {estimator}: {T} steps", flush=True)
+    for t in range(T):
+        ll.ll_masks(n, P, t, ll.LL_DIR_GRAD, spec, masks)
+        ll.lossy_aggregate(grads, masks, d=d, packet=L, g_hat=g_hat, ext=e)
+        acc += g_hat.double()
+    mc = (acc / T).cpu().numpy()
+    g64 = g.astype(np.float64)
+    for k in range(P):
+        sl = slice(k * L, (k + 1) * L)
+        mean, var = _exact_moments(g64[:, sl], p, estimator)
+        err = np.abs(mc[sl] - mean)
+        bound = 5.5 * np.sqrt(var / T) + 1e-12
+        assert (err <= bound).all(), (k, float((err / bound).max()))
+        if estimator == "horvitz_thompson":
+            assert np.allclose(mean, g64[:, sl].mean(axis=0), atol=1e-12)
+        else:
+            assert np.allclose(mean, (1 - p**n) * g64[:, sl].mean(axis=0), atol=1e-12)
+
+
+def test_worker_lost_for_good():
+    # A worker whose transfers never arrive, in both directions, for 30 steps:
+    # its gradient row holds NaN and is never read; its replica keeps the
+    # initial values bit for bit; the others follow the masks.
+    n, L, P, dead = 6, 512, 10, 4
+    d = L * P - 100
+    rng = np.random.default_rng(5)
+    theta = torch.from_numpy((rng.standard_normal(d) * 0.02).astype(np.float32)).to(DEV)
+    ld = (d + 7) // 8 * 8
+    rep0 = torch.zeros((n, ld), dtype=torch.bfloat16, device=DEV)[:, :d]
+    rep0[:] = theta.to(torch.bfloat16)[None, :]
+    replicas = torch.zeros((n, ld), dtype=torch.bfloat16, device=DEV)[:, :d]
+    replicas.copy_(rep0)
+    grads = torch.empty((n, ld), dtype=torch.bfloat16, device=DEV)[:, :d]
+    mg = torch.empty((n, P), dtype=torch.uint8, device=DEV)
+    mb = torch.empty_like(mg)
+    g_hat = torch.empty(d, dtype=torch.float32, device=DEV)
+    spec = ll.bernoulli(0.2, seed=9)
+    opt = ll.sgd(1e-2)
+    for t in range(30):
+        grads.copy_(torch.from_numpy(rng.standard_normal((n, d)).astype(np.float32)).to(torch.bfloat16))
+        grads[dead] = float("nan")
+        ll.ll_masks(n, P, t, ll.LL_DIR_GRAD, spec, mg)
+        ll.ll_masks(n, P, t, ll.LL_DIR_BCAST, spec, mb)
+        mg[dead] = 0
+        mb[dead] = 0
+        ll.lossy_aggregate(grads, mg, d=d, packet=L, g_hat=g_hat)
+        assert torch.isfinite(g_hat).all(), f"step {t}: the dead row was read"
+        ll.shard_step(opt, t, theta, g_hat)
+        ll.lossy_broadcast(theta, replicas, mb, d=d, packet=L)
+    assert torch.equal(replicas[dead].view(torch.int16), rep0[dead].view(torch.int16))
+    R = mb.repeat_interleave(L, dim=1)[:, :d].bool()
+    own = theta.to(torch.bfloat16)[None, :].expand(n, -1)
+    assert torch.equal(replicas[R].view(torch.int16), own[R].view(torch.int16))
