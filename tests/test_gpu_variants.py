@@ -336,3 +336,50 @@ def test_fused_parity_masks_in_workspace_match_masks_out():
         for k in ("theta", "m", "v", "replicas"):
             assert torch.equal(getattr(a, k).view(torch.uint8), getattr(b, k).view(torch.uint8)), k
         assert ll.read_drift(a.drift) == ll.read_drift(b.drift)
+
+
+@pytest.mark.parametrize("est", ["horvitz_thompson", "stale_fill"])
+def test_all_variants_at_once_with_oracle(est):
+    # Owner row, reliable packets, parity packets, ages and an estimator
+    # variant together.  Horvitz-Thompson takes an explicit q here (with
+    # reliable packets inside the groups no single q is exact); the oracle
+    # is given the same weights, so the comparison is of the arithmetic.
+    G, owner = 3, 2
+    w = wl.scaled(wl.WORKLOADS["n8_d16m_bf16_adam"], d=2048 * 45 + 40, steps=3,
+                  loss=dict(kind=wl.BERNOULLI, p=0.35))
+    print(f"all variants {est}", flush=True)
+    dev = parity.DeviceState(w, pad=8)
+    relf, relt, prev, ages = _variant_setup(w, est, owner, True, dev)
+    p = w.loss["p"]
+    q_hat = oloss.parity_arrival_probability(1 - p, G)
+    e = ll.ext(estimator=est, owner=owner, reliable=relt, g_prev=prev, ages=ages,
+               arrival_prob=q_hat if est == "horvitz_thompson" else 0.0, parity_group=G)
+    packets = list(range(w.num_packets))
+    so = parity.SampledOracle(w, packets, dev)
+    prev_o = np.zeros((w.n, w.d), np.uint16)
+    ages_o = np.zeros((w.n, w.num_packets), np.uint16)
+    q = np.full((w.n, w.num_packets), q_hat)
+    q[owner] = 1.0
+    q[:, relf.astype(bool)] = 1.0
+    for t in range(w.steps):
+        if t > 0:
+            wl.draw_grads(w, t, device=DEV, ld=dev.ld, out=dev.grads)
+        g_host = parity.host_rows(dev.grads, so.idx, w.gdtype)
+        dev.fused(t, ext=e)
+        mg = _parity_masks(w.seed, t, 0, w.n, w.num_packets, p, G, owner, relf)
+        mb = _parity_masks(w.seed, t, 1, w.n, w.num_packets, p, G, owner, relf)
+        assert np.array_equal(dev.arrived_g.cpu().numpy(), mg), f"step {t}"
+        assert np.array_equal(dev.arrived_b.cpu().numpy(), mb), f"step {t}"
+        orc = ostep.lossy_step(d=w.d, packet=w.packet, packets=packets, gdtype=w.gdtype,
+                               grads=g_host, theta=so.theta, m=so.m, v=so.v,
+                               replicas=so.replicas, arrived_g=mg, arrived_b=mb, opt=w.opt, t=t,
+                               estimator=est, q=q, g_prev=prev_o)
+        so.prev_replicas = so.replicas
+        so.theta, so.m, so.v, so.replicas = orc["theta"], orc["m"], orc["v"], orc["replicas"]
+        parity.compare_step(w, t, dev, so, orc, mb, f"all variants {est} step {t}")
+        ages_o = ostep.update_ages(ages_o, mb)
+        assert np.array_equal(_ages_host(ages), ages_o), f"step {t}: ages"
+        if est == "stale_fill":
+            prev_o = orc["g_prev"]
+            assert np.array_equal(parity.host_rows(prev, so.idx, w.gdtype), prev_o)
+        so.upload(dev)
