@@ -23,8 +23,10 @@
  *     all memory; the library allocates none.  Scratch memory comes from a
  *     caller-supplied workspace of ll_workspace_bytes() bytes.
  *   - `stream` is a hipStream_t (NULL = the default stream).  Every call only
- *     enqueues work on it and returns without synchronising; device outputs
- *     are valid once the stream has reached that point.
+ *     enqueues kernels on it (no allocation, no memset, no copy) and returns
+ *     without synchronising; device outputs are valid once the stream has
+ *     reached that point.  Calls can therefore be captured into a HIP graph;
+ *     a replay repeats the captured step index.
  *   - Row-major [N][ld] buffers: row i starts at element i * ld.  ld >= D.
  *   - Masks are uint8 [N][P] (row i = worker/replica i, column k = packet),
  *     1 = arrived, 0 = lost.
