@@ -10,7 +10,14 @@ Orda, 2025) defines for one owner's shard:
     fallback when nothing arrives;
   * Section 3 step (3): the owner's local update (plus momentum and Adam);
   * Section 3 step (4): the lossy broadcast that keeps stale values;
-  * Theorem 3.1: the inter-replica discrepancy D = theta^(i,j) - theta^(k,j).
+  * Theorem 3.1: the inter-replica discrepancy D = theta^(i,j) - theta^(k,j);
+  * Algorithm 1's gradient half: a lost contribution replaced by the last one
+    that arrived, averaged over N (stale fill);
+  * Section 5 directions: transfers that cannot be lost (the owner's own row,
+    reliable packets), XOR parity packets over groups of packets, and the
+    per-replica record of broadcast ages (the routing log);
+  * beyond the paper: a Horvitz-Thompson form of the aggregate and bursty
+    Gilbert-Elliott loss (Section 5 names bursty loss as open).
 
 It shares no code with the HIP library and never imports it.  Only the test
 suite, the smoke entry point and the benchmark's CPU-baseline leg may import
