@@ -212,11 +212,11 @@ int make_parity(const ExtView& x, int32_t n, int64_t P, uint64_t step, ParityLau
     L->ndir = 0;
     L->n = n;
     L->G = x.parity;
+    L->span = x.parity * (kThreads / x.parity);
     L->P = P;
-    L->groups = (P + x.parity - 1) / x.parity;
+    L->spans = (P + L->span - 1) / L->span;
     L->step = step;
-    if ((2 * (int64_t)n * L->groups + kThreads - 1) / kThreads > 0x7FFFFFFFll)
-        return fail(LL_EINVAL, "too many workgroups");
+    if (2 * (int64_t)n * L->spans > 0x7FFFFFFFll) return fail(LL_EINVAL, "too many workgroups");
     return LL_OK;
 }
 

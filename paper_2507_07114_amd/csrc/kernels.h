@@ -142,9 +142,11 @@ struct ParityJob {
     uint8_t* arrived;         // [n][P] out
 };
 
+// A workgroup covers `span` consecutive packets of one row, span = G *
+// floor(kThreads / G), so groups never straddle workgroups.
 struct ParityLaunch {
-    int ndir, n, G;
-    int64_t P, groups;  // groups = ceil(P / G) per row
+    int ndir, n, G, span;
+    int64_t P, spans;  // spans = ceil(P / span) per row
     uint64_t step;
     ParityJob job[2];
 };

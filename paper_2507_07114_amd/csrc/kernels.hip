@@ -33,37 +33,58 @@ __global__ __launch_bounds__(kThreads) void k_masks_bernoulli(int n, int64_t num
     }
 }
 
-// Bernoulli masks with parity packets: one thread per (direction, row, group
-// of G packets).  It draws the group's arrivals, applies the transfers that
-// cannot be lost, and when exactly one packet is missing and the group's
-// parity packet (counter (group, row, step, dir + 2)) arrived, marks that
-// packet arrived: XOR of the parity with the other G - 1 packets rebuilds it
-// exactly.
+// Bernoulli masks with parity packets.  A workgroup takes `span` consecutive
+// packets of one (direction, row), one packet per thread, span a multiple of
+// G.  Each thread draws its packet's arrival and applies the transfers that
+// cannot be lost, and the first span / G threads draw the arrival of one
+// group's parity packet each (counter (group, row, step, dir + 2)); ballots
+// put both bitmaps in LDS.  A lost packet whose group (G consecutive packets)
+// lost nothing else is rebuilt when the group's parity packet arrived: XOR
+// of the parity with the other G - 1 packets gives it back exactly.
 __global__ __launch_bounds__(kThreads) void k_masks_parity(ParityLaunch L) {
-    const int64_t per_dir = (int64_t)L.n * L.groups;
-    const int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x;
-    if (idx >= L.ndir * per_dir) return;
-    const int s = idx >= per_dir ? 1 : 0;
+    __shared__ uint64_t s_lost[kThreads / 64];
+    __shared__ uint64_t s_par[kThreads / 64];
+    const int64_t per_dir = (int64_t)L.n * L.spans;
+    const int64_t b = blockIdx.x;
+    const int s = b >= per_dir ? 1 : 0;
     const ParityJob& J = L.job[s];
-    const int64_t rem = idx - s * per_dir;
-    const int64_t i = rem / L.groups;
-    const int64_t j = rem - i * L.groups;
-    const int64_t k0 = j * L.G;
-    const int64_t k1 = k0 + L.G < L.P ? k0 + L.G : L.P;
-    uint8_t* row = J.arrived + i * L.P;
-    int64_t missing = 0, last = -1;
-    for (int64_t k = k0; k < k1; ++k) {
-        const bool a = bernoulli_arrived((uint64_t)k, (uint64_t)i, L.step, J.dir, J.seed, J.thr) ||
-                       forced_arrival((int)i, k, J.owner, J.reliable);
-        row[k] = a ? 1 : 0;
-        if (!a) {
-            ++missing;
-            last = k;
-        }
+    const int64_t rem = b - s * per_dir;
+    const int64_t i = rem / L.spans;
+    const int64_t k0 = (rem - i * L.spans) * L.span;
+    const int t = threadIdx.x;
+    const int64_t k = k0 + t;
+    const bool in = t < L.span && k < L.P;
+    bool a = true;
+    if (in)
+        a = bernoulli_arrived((uint64_t)k, (uint64_t)i, L.step, J.dir, J.seed, J.thr) ||
+            forced_arrival((int)i, k, J.owner, J.reliable);
+    // thread t < span / G: parity packet of group k0 / G + t (if the group exists)
+    bool par = false;
+    if (t < L.span / L.G && k0 + (int64_t)t * L.G < L.P)
+        par = bernoulli_arrived((uint64_t)(k0 / L.G + t), (uint64_t)i, L.step, J.dir + 2, J.seed,
+                                J.thr);
+    const uint64_t lost = __ballot(!a);
+    const uint64_t pbits = __ballot(par);
+    if ((t & 63) == 0) {
+        s_lost[t >> 6] = lost;
+        s_par[t >> 6] = pbits;
     }
-    if (missing == 1 &&
-        bernoulli_arrived((uint64_t)j, (uint64_t)i, L.step, J.dir + 2, J.seed, J.thr))
-        row[last] = 1;
+    __syncthreads();
+    if (!in) return;
+    if (!a) {
+        const int gl = t / L.G;                                // group within the span
+        const int g0 = gl * L.G;                               // its first thread
+        const int g1 = g0 + L.G < L.span ? g0 + L.G : L.span;  // one past its last
+        int missing = 0;
+        for (int w = g0 >> 6; w <= (g1 - 1) >> 6; ++w) {
+            const int lo = g0 > w * 64 ? g0 - w * 64 : 0;
+            const int hi = g1 < (w + 1) * 64 ? g1 - w * 64 : 64;
+            const uint64_t keep = (hi == 64 ? ~0ull : ((1ull << hi) - 1)) & ~((1ull << lo) - 1);
+            missing += __popcll(s_lost[w] & keep);
+        }
+        if (missing == 1) a = (s_par[gl >> 6] >> (gl & 63)) & 1;
+    }
+    J.arrived[i * L.P + k] = a ? 1 : 0;
 }
 
 // Gilbert-Elliott masks.  A chain's per-packet transition is a map on
@@ -503,8 +524,7 @@ hipError_t launch_masks_bernoulli(int n, int64_t num_packets, uint64_t step, int
 }
 
 hipError_t launch_masks_parity(const ParityLaunch& L, hipStream_t s) {
-    const int64_t total = (int64_t)L.ndir * L.n * L.groups;
-    const int64_t blocks = (total + kThreads - 1) / kThreads;
+    const int64_t blocks = (int64_t)L.ndir * L.n * L.spans;
     hipLaunchKernelGGL(k_masks_parity, dim3((unsigned)blocks), dim3(kThreads), 0, s, L);
     return hipGetLastError();
 }
