@@ -206,7 +206,13 @@ def main():
     ap.add_argument("--ages", action="store_true", help="track broadcast ages")
     ap.add_argument("--parity-group", type=int, default=0,
                     help="packets per XOR parity packet (0: no parity packets)")
+    ap.add_argument("--stagewise", action="store_true",
+                    help="time the chain of one-stage entry points (ll_masks, lossy_aggregate, "
+                         "shard_step, lossy_broadcast, drift_stats) instead of the fused step")
     args = ap.parse_args()
+    if args.stagewise and (args.estimator != "arrived_mean" or args.owner >= 0
+                           or args.reliable_every > 0 or args.ages or args.parity_group > 0):
+        ap.error("--stagewise times the default step only")
     variant = (args.estimator != "arrived_mean" or args.owner >= 0 or args.reliable_every > 0
                or args.ages or args.parity_group > 0)
 
@@ -281,8 +287,25 @@ def main():
                 w, mg_dev.cpu().numpy(), mb_dev.cpu().numpy(), lens, True,
                 estimator=args.estimator, ages=args.ages, reliable=rel_np is not None))
 
+    step_fn = (lambda t: dev.fused(t, masks_out=False, ext=ext))
+    if args.stagewise:
+        from workloads.device import opt_spec
+        g_hat = torch.empty(w.d, dtype=torch.float32, device="cuda")
+
+        def step_fn(t):
+            ll.ll_masks(w.n, P, t, ll.LL_DIR_GRAD, spec, dev.arrived_g, ge_state=dev.ge_g,
+                        workspace=dev.workspace)
+            ll.lossy_aggregate(dev.grads, dev.arrived_g, d=w.d, packet=w.packet, g_hat=g_hat,
+                               counts=dev.counts, theta=dev.theta)
+            ll.shard_step(opt_spec(w), t, dev.theta, g_hat, m=dev.m, v=dev.v)
+            ll.ll_masks(w.n, P, t, ll.LL_DIR_BCAST, spec, dev.arrived_b, ge_state=dev.ge_b,
+                        workspace=dev.workspace)
+            ll.lossy_broadcast(dev.theta, dev.replicas, dev.arrived_b, d=w.d, packet=w.packet)
+            ll.drift_stats(dev.replicas, d=w.d, packet=w.packet, workspace=dev.workspace,
+                           out=dev.drift, theta=dev.theta, arrived_bc=dev.arrived_b)
+
     for t in range(args.warmup):
-        dev.fused(t, masks_out=False, ext=ext)
+        step_fn(t)
     torch.cuda.synchronize()
 
     # A workload smaller than the 256 MB memory-side cache (MALL) would be
@@ -303,7 +326,7 @@ def main():
         if mall_flush:
             scratch.fill_(float(j))
         starts[j].record(stream)
-        dev.fused(args.warmup + j, masks_out=False, ext=ext)
+        step_fn(args.warmup + j)
         ends[j].record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
@@ -319,7 +342,7 @@ def main():
     launch_ms = float(np.mean(ms))
     achieved = mean_bytes / (launch_ms * 1e-3) / 1e9
     khash = kernel_source_hash()
-    traffic = read_pmc_traffic(khash)
+    traffic = None if args.stagewise else read_pmc_traffic(khash)
     mean_b = {k: int(np.mean([b[k] for b in per_step_bytes])) for k in per_step_bytes[0]}
     log(f"per-launch event times (ms): min {min(ms):.3f} median {float(np.median(ms)):.3f} "
         f"max {max(ms):.3f}; algorithmic bytes/step {mean_b}")
@@ -343,7 +366,8 @@ def main():
                    "drift": True, "parallelism": "single-gpu simulation of n workers",
                    "estimator": args.estimator, "owner": args.owner,
                    "reliable_every": args.reliable_every, "ages": args.ages,
-                   "parity_group": args.parity_group, "footprint_bytes": footprint,
+                   "parity_group": args.parity_group, "stagewise": args.stagewise,
+                   "footprint_bytes": footprint,
                    "mall_flush_between_steps": mall_flush},
         "pct_hbm_peak": round(100.0 * value / HBM_PEAK_GBS, 2),
         "elements_per_s": round(w.n * w.d / (ms_per_step * 1e-3), 1),
@@ -355,7 +379,9 @@ def main():
         "hbm_copy_probe_gbs": round(copy_gbs, 1),
         "roofline": {
             "bound": "hbm",
-            "kernel": "k_step_fused (+ k_drift_reduce, k_drift_final)",
+            "kernel": ("stage chain: masks x2, k_aggregate, k_shard_step, k_broadcast, k_drift "
+                       "(+ reductions)") if args.stagewise else
+                      "k_step_fused (+ k_drift_reduce, k_drift_final)",
             "achieved": round(achieved, 2),
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
