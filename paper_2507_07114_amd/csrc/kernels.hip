@@ -315,15 +315,15 @@ __global__ __launch_bounds__(R::kPacketThreads) void k_drift(DriftParams p) {
         }
         Drift8 acc;
         acc.init(false, r);
-        for (int i0 = 0; i0 < p.n; i0 += kBatchStale) {
-            float x[kBatchStale][8];
+        for (int i0 = 0; i0 < p.n; i0 += kBatchDrift) {
+            float x[kBatchDrift][8];
 #pragma unroll
-            for (int u = 0; u < kBatchStale; ++u) {
+            for (int u = 0; u < kBatchDrift; ++u) {
                 const int row = i0 + u < p.n ? i0 + u : i0;
                 load8<R>(reps + (int64_t)row * p.ld + ch.e0, ch.nv, x[u]);
             }
 #pragma unroll
-            for (int u = 0; u < kBatchStale; ++u)
+            for (int u = 0; u < kBatchDrift; ++u)
                 if (i0 + u < p.n) acc.add(x[u], r, ch.nv);
         }
         acc.finish(p.n, ch.nv, pair, range);
