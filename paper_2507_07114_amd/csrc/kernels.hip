@@ -1,10 +1,12 @@
 // HIP kernels of the lossy step for gfx950 and their launchers.
 //
-// Work decomposition shared by every per-packet kernel: one workgroup of 256
-// threads (4 wave64s) owns a chunk of up to 2048 consecutive elements of one
-// packet; thread t owns elements [8t, 8t + 8) of the chunk, so each row read
-// or written is one 16-byte (bf16) or two 16-byte (fp32) accesses per thread
-// and a wavefront touches 1 KiB (bf16) or 2 KiB (fp32) of contiguous HBM.
+// Work decomposition shared by every per-packet kernel: a workgroup owns a
+// chunk of one packet covering 4 KiB of each row it streams (256 threads =
+// 4 wave64s and 2048 elements for bf16 rows, 128 threads and 1024 elements
+// for fp32 rows); thread t owns elements [8t, 8t + 8) of the chunk, so each
+// row read or written is one 16-byte (bf16) or two 16-byte (fp32) accesses
+// per thread and a wavefront touches 1 KiB (bf16) or 2 KiB (fp32) of
+// contiguous HBM.
 // The masks of the packet sit in LDS as 64-bit words; loops over arrived or
 // stale rows walk the set bits with scalar (wave-uniform) control flow, so
 // a lost packet costs no memory traffic and causes no divergence.
