@@ -143,3 +143,36 @@ def test_drift_workload_all_steps_on_a_packet_slice():
     finally:
         del dev
         _free()
+
+
+def test_drift_stays_bounded_over_two_thousand_steps():
+    # Theorem 3.1's claim over a long horizon: 2000 steps of N = 64 replicas
+    # (a 409,600-element slice of the drift workload's shape).  The mean
+    # squared discrepancy per unit of master movement is the same in each
+    # 500-step window and equals 2p / (1 - p^2).
+    w = wl.scaled(wl.WORKLOADS["n64_d48m_f32_sgd_drift"], d=2048 * 200, steps=2000)
+    p = w.loss["p"]
+    dev = parity.DeviceState(w)
+    prev = dev.theta.clone()
+    ratio = []
+    try:
+        for t in range(w.steps):
+            if t > 0:
+                wl.draw_grads(w, t, device=DEV, ld=dev.ld, out=dev.grads)
+            dev.fused(t)
+            step = (dev.theta - prev).double().square().mean()
+            prev.copy_(dev.theta)
+            ratio.append((ll.read_drift(dev.drift)["mean_sq"], float(step)))
+            if t % 500 == 0:
+                print(f"  step {t}: mean_sq {ratio[-1][0]:.3e}", flush=True)
+    finally:
+        del dev
+        _free()
+    ms = np.array([r[0] for r in ratio])
+    s2 = np.array([r[1] for r in ratio])
+    corrected = 2 * p / (1 - p * p)
+    windows = [float(ms[a:a + 500].mean() / s2[a:a + 500].mean()) for a in range(0, 2000, 500)]
+    print(f"E[D^2]/sigma^2 per 500-step window: {windows}; 2p/(1-p^2) = {corrected:.4f}", flush=True)
+    for r in windows[1:]:   # the first window includes the burn-in from identical replicas
+        assert abs(r - corrected) < 0.04 * corrected
+    assert max(windows[1:]) - min(windows[1:]) < 0.04 * corrected
