@@ -17,11 +17,15 @@ from typing import Optional
 import torch
 
 __all__ = [
-    "LossSpec", "OptSpec", "bernoulli", "gilbert_elliott", "sgd", "sgd_momentum", "adam",
-    "ll_masks", "ll_ages_update", "lossy_aggregate", "Ext", "ext", "ESTIMATORS", "shard_step", "lossy_broadcast", "drift_stats",
-    "lossy_step_fused", "ll_workspace_bytes", "ll_masks_workspace_bytes", "ll_last_error",
-    "drift_buffer",
-    "read_drift", "library_path", "LossyError",
+    # entry points of include/lossy.h
+    "ll_masks", "ll_ages_update", "lossy_aggregate", "shard_step", "lossy_broadcast",
+    "drift_stats", "lossy_step_fused", "ll_workspace_bytes", "ll_masks_workspace_bytes",
+    "ll_last_error",
+    # argument structs and their builders
+    "LossSpec", "OptSpec", "Ext", "bernoulli", "gilbert_elliott", "sgd", "sgd_momentum", "adam",
+    "ext", "ESTIMATORS",
+    # helpers
+    "drift_buffer", "read_drift", "library_path", "LossyError",
     "LL_F32", "LL_BF16", "LL_DIR_GRAD", "LL_DIR_BCAST",
 ]
 
