@@ -142,3 +142,23 @@ def parity_arrival_probability(q: float, group: int) -> float:
     or it alone was lost and the other group - 1 packets and the parity
     packet arrived."""
     return q + (1.0 - q) * q**group
+
+
+def parity_arrival_probabilities(q: float, group: int, num_packets: int, reliable=None):
+    """Marginal arrival probability of every packet of a row under parity
+    packets, float64 [num_packets].  A reliable packet always arrives (1).  A
+    lossy packet k in a group of size g_k (the last group may be shorter)
+    with r_k reliable other members arrives, or was lost while the other
+    g_k - 1 - r_k lossy members and the parity packet arrived:
+    q + (1 - q) q^(g_k - r_k)."""
+    rel = np.zeros(num_packets, bool) if reliable is None else np.asarray(reliable).astype(bool)
+    out = np.empty(num_packets)
+    for k in range(num_packets):
+        if rel[k]:
+            out[k] = 1.0
+            continue
+        lo = (k // group) * group
+        hi = min(lo + group, num_packets)
+        r = int(rel[lo:hi].sum())  # k itself is not reliable
+        out[k] = q + (1.0 - q) * q ** (hi - lo - r)
+    return out

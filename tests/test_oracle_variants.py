@@ -239,3 +239,25 @@ def test_parity_respects_overrides_and_ragged_tail():
     assert out.tolist() == [[1] * 7, [1] * 7]
     par[0, 2] = 0
     assert loss.parity_recover(s, 3, par)[0, 6] == 0
+
+
+@pytest.mark.parametrize("G,P,rel", [(3, 7, [0, 1, 0, 0, 0, 1, 0]), (4, 4, None), (2, 5, [1, 0, 0, 0, 1])])
+def test_parity_marginals_with_reliable_and_ragged_groups_by_enumeration(G, P, rel):
+    # Exact marginals over every loss pattern of the lossy packets and every
+    # group's parity packet (reliable packets never lost).
+    q = 0.6
+    relf = np.zeros(P, np.uint8) if rel is None else np.array(rel, np.uint8)
+    lossy = [k for k in range(P) if not relf[k]]
+    ngroups = (P + G - 1) // G
+    marg = np.zeros(P)
+    for bits in itertools.product((0, 1), repeat=len(lossy) + ngroups):
+        a = np.ones((1, P), np.uint8)
+        for b, k in zip(bits[: len(lossy)], lossy):
+            a[0, k] = b
+        par = np.array([bits[len(lossy):]], np.uint8)
+        pr = np.prod([q if b else 1 - q for b in bits])
+        marg += pr * loss.parity_recover(loss.apply_overrides(a, reliable=relf), G, par)[0]
+    want = loss.parity_arrival_probabilities(q, G, P, None if rel is None else relf)
+    assert np.allclose(marg, want, atol=1e-14)
+    if rel is None and P % G == 0:
+        assert np.allclose(want, loss.parity_arrival_probability(q, G), atol=1e-15)
