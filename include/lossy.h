@@ -154,9 +154,9 @@ typedef struct {
  *                 (0 = this step; saturates at 65535).
  *   arrival_prob  q of LL_EST_HORVITZ_THOMPSON in (0, 1].  lossy_aggregate
  *                 requires it; lossy_step_fused takes 0 to mean the arrival
- *                 probability of a Bernoulli gradient loss: 1 - p, or with
- *                 parity packets q + (1 - q) q^G (q = 1 - p), which needs
- *                 reliable == NULL and P a multiple of G.
+ *                 probability of a Bernoulli gradient loss: q = 1 - p, or with
+ *                 parity packets each packet's own q + (1 - q) q^(g - r), g
+ *                 the size of its group and r the reliable other members.
  *   parity_group  0 (none), or G in [1, 256]: erasure coding over groups of G
  *                 consecutive packets (the parity packets proposed in the
  *                 paper's Section 5).  Per row and group, the sender adds one

@@ -239,6 +239,8 @@ int make_variant(const ExtView& x, double q, const void* g_prev_checked, AggVari
     v->reliable = x.reliable;
     v->g_prev = const_cast<void*>(g_prev_checked);
     v->invq = 1.0f;
+    v->parity_group = 0;
+    v->q = q;
     if (x.est == LL_EST_HORVITZ_THOMPSON) {
         if (!(q > 0.0 && q <= 1.0))
             return fail(LL_EINVAL, "Horvitz-Thompson needs an arrival probability in (0, 1]");
@@ -481,18 +483,13 @@ int lossy_step_fused(int32_t n, int64_t d, int64_t packet, uint64_t step, const 
         if (loss_g->kind != LL_LOSS_BERNOULLI)
             return fail(LL_EINVAL, "Horvitz-Thompson under Gilbert-Elliott loss needs arrival_prob");
         q = 1.0 - loss_g->p;
-        if (x.parity) {
-            // A packet also arrives when it alone was lost in its group and
-            // the parity packet came through: q + (1 - q) q^G, the same for
-            // every packet only when all groups are full and none is reliable.
-            if (x.reliable || g.P % x.parity != 0)
-                return fail(LL_EINVAL, "Horvitz-Thompson with parity packets needs arrival_prob "
-                                       "unless P is a multiple of parity_group and reliable is NULL");
-            q = q + (1.0 - q) * std::pow(q, (double)x.parity);
-        }
     }
     AggVariant var;
     if ((r = make_variant(x, q, x.g_prev, &var))) return r;
+    // With parity packets and a derived q, a packet also arrives when it
+    // alone was lost in its group and the parity packet came through; the
+    // kernel turns q into each packet's probability from its group.
+    if (x.est == LL_EST_HORVITZ_THOMPSON && x.q == 0.0 && x.parity) var.parity_group = x.parity;
     const WsLayout w = ws_layout(n, g);
     const bool need_ws = drift || ge_g || ge_b || x.parity;
     if (need_ws) {

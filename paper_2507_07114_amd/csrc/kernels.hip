@@ -437,8 +437,10 @@ __global__ __launch_bounds__(R::kPacketThreads) void k_step_fused(FusedParams p)
         if (p.opt.kind >= 1) load_f32x8(p.m + ch.e0, ch.nv, mm);
         if (p.opt.kind == 2) load_f32x8(p.v + ch.e0, ch.nv, vv);
         const bool relp = p.var.reliable != nullptr && p.var.reliable[ch.k] != 0;
+        AggVariant var = p.var;
+        if (var.parity_group > 0 && !relp) var.invq = parity_invq(var, ch.k, p.P);
         aggregate8<G>(reinterpret_cast<const typename G::T*>(p.grads), p.ld_g, ch.e0, ch.nv,
-                      s_words[0], nw, p.n, K, p.lam, th, p.var, relp, g);
+                      s_words[0], nw, p.n, K, p.lam, th, var, relp, g);
         update8(p.opt, th, mm, vv, g);
         store_f32x8(p.theta + ch.e0, ch.nv, th);
         if (p.opt.kind >= 1) store_f32x8(p.m + ch.e0, ch.nv, mm);

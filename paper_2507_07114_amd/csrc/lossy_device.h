@@ -260,7 +260,26 @@ struct AggVariant {
     float invq;               // 1 / arrival probability (Horvitz-Thompson)
     const uint8_t* reliable;  // [P] packets that cannot be lost, or null
     void* g_prev;             // [n][ld] last arrived contributions (stale fill)
+    // Horvitz-Thompson under parity packets with the arrival probability
+    // derived per packet: group size (0 = use invq as given) and q.
+    int parity_group;
+    double q;
 };
+
+// 1 / arrival probability of lossy packet k (of P) of a row under parity
+// packets: it arrives, or it alone was lost in its group of g packets (the
+// last group may be shorter) while the g - 1 - r other lossy members (r =
+// reliable others) and the group's parity packet arrived: q + (1 - q) q^(g - r).
+__device__ __forceinline__ float parity_invq(const AggVariant& v, int64_t k, int64_t P) {
+    const int64_t g0 = (k / v.parity_group) * v.parity_group;
+    const int64_t g1 = g0 + v.parity_group < P ? g0 + v.parity_group : P;
+    int r = 0;
+    if (v.reliable)
+        for (int64_t j = g0; j < g1; ++j) r += (j != k && v.reliable[j] != 0) ? 1 : 0;
+    double qn = 1.0;
+    for (int64_t e = 0; e < g1 - g0 - r; ++e) qn *= v.q;
+    return (float)(1.0 / (v.q + (1.0 - v.q) * qn));
+}
 
 // Arrived mean (Section 3 step (2)): g = (sum over arrived rows, ascending, in
 // fp32) / K, or lam * theta when K = 0.

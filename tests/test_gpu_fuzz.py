@@ -26,7 +26,7 @@ OPTS = {
 }
 
 
-def _cases(count=64, seed=2026):
+def _cases(count=96, seed=2026):
     rng = np.random.default_rng(seed)
     out = []
     for c in range(count):
@@ -47,8 +47,7 @@ def _cases(count=64, seed=2026):
             est = "arrived_mean"
         owner = int(rng.integers(0, n)) if rng.random() < 0.3 else -1
         reliable = bool(rng.random() < 0.3)
-        parity_g = int(rng.choice([1, 2, 5, 16])) if (bern and est != "horvitz_thompson"
-                                                     and rng.random() < 0.3) else 0
+        parity_g = int(rng.choice([1, 2, 5, 16])) if (bern and rng.random() < 0.3) else 0
         lam = 0.1 if (est == "arrived_mean" and rng.random() < 0.3) else 0.0
         out.append(dict(case=c, n=n, packet=packet, d=d, gdtype=gdtype, opt=opt, loss=loss,
                         est=est, owner=owner, reliable=reliable, parity=parity_g, lam=lam))
@@ -94,11 +93,18 @@ def test_random_configuration(cfg):
         pi_bad = l["p_gb"] / (l["p_gb"] + l["p_bg"])
         q_lossy = 1 - pi_bad * l["loss_bad"] - (1 - pi_bad) * l["loss_good"]
     prev = torch.zeros_like(dev.grads) if est == "stale_fill" else None
+    # Bernoulli: the fused step derives q (per packet under parity packets);
+    # Gilbert-Elliott: the chain's stationary arrival probability is given.
+    derived = l["kind"] == wl.BERNOULLI
     e = ll.ext(estimator=est, owner=owner,
                reliable=None if relf is None else torch.from_numpy(relf).to(DEV),
-               g_prev=prev, arrival_prob=q_lossy if est == "horvitz_thompson" else 0.0,
+               g_prev=prev,
+               arrival_prob=q_lossy if (est == "horvitz_thompson" and not derived) else 0.0,
                parity_group=G)
-    q = np.full((w.n, P), q_lossy)
+    if derived and G:
+        q = np.tile(oloss.parity_arrival_probabilities(q_lossy, G, P, relf), (w.n, 1))
+    else:
+        q = np.full((w.n, P), q_lossy)
     if owner >= 0:
         q[owner] = 1.0
     if relf is not None:

@@ -281,12 +281,14 @@ def test_parity_masks_bit_exact(G, n, P, owner, rel):
 
 @pytest.mark.parametrize("est,G,owner,rel", [
     ("arrived_mean", 4, -1, False), ("arrived_mean", 3, 1, True),
-    ("horvitz_thompson", 6, -1, False), ("stale_fill", 2, 0, False),
+    ("horvitz_thompson", 6, -1, False), ("horvitz_thompson", 4, 2, True),
+    ("stale_fill", 2, 0, False),
 ])
 def test_fused_parity_with_oracle(est, G, owner, rel):
     # 2048 * 60 + 24 elements in packets of 2048: 61 packets, the last ragged
-    # (a multiple of G only for G = 1, so Horvitz-Thompson runs on 60 packets).
-    d = 2048 * 60 + (0 if est == "horvitz_thompson" else 24)
+    # (G = 6 with Horvitz-Thompson runs on 60 full-group packets; G = 4 with
+    # reliable packets and the ragged tail takes each packet's own q).
+    d = 2048 * 60 + (0 if (est, G) == ("horvitz_thompson", 6) else 24)
     w = wl.scaled(wl.WORKLOADS["n8_d16m_bf16_adam"], d=d, steps=3,
                   loss=dict(kind=wl.BERNOULLI, p=0.3))
     print(f"fused parity {est} G={G} owner={owner} rel={rel}", flush=True)
@@ -297,7 +299,7 @@ def test_fused_parity_with_oracle(est, G, owner, rel):
     so = parity.SampledOracle(w, packets, dev)
     prev_o = np.zeros((w.n, w.d), np.uint16)
     p = w.loss["p"]
-    q = np.full((w.n, w.num_packets), oloss.parity_arrival_probability(1 - p, G))
+    q = np.tile(oloss.parity_arrival_probabilities(1 - p, G, w.num_packets, relf), (w.n, 1))
     if owner >= 0:
         q[owner] = 1.0
     for t in range(w.steps):
