@@ -223,7 +223,7 @@ def main():
                or args.ages or args.parity_group > 0)
 
     if args.gpus != 1:
-        print(f"bench.py measures one GPU only: this build simulates the N workers of one "
+        print(f"bench.py measures one GPU only: the library simulates the N workers of one "
               f"owner's shard on a single device and has no multi-GPU path "
               f"(asked for --gpus {args.gpus}).", file=sys.stderr)
         sys.exit(2)
