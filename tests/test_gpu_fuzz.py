@@ -55,6 +55,18 @@ def _cases(count=96, seed=2026):
 
 
 CASES = _cases()
+# the largest worker count, on every path of the kernel that depends on it
+CASES += [
+    dict(case=1000, n=1024, packet=512, d=3000, gdtype=wl.BF16, opt="adam",
+         loss=dict(kind=wl.BERNOULLI, p=0.3), est="horvitz_thompson", owner=1023,
+         reliable=True, parity=3, lam=0.0),
+    dict(case=1001, n=1024, packet=1000, d=2500, gdtype=wl.F32, opt="momentum",
+         loss=dict(kind=wl.GILBERT_ELLIOTT, p_gb=0.3, p_bg=0.2, loss_good=0.0, loss_bad=1.0),
+         est="stale_fill", owner=-1, reliable=False, parity=0, lam=0.0),
+    dict(case=1002, n=1024, packet=8, d=77, gdtype=wl.BF16, opt="sgd",
+         loss=dict(kind=wl.BERNOULLI, p=0.95), est="arrived_mean", owner=-1,
+         reliable=False, parity=1, lam=0.1),
+]
 
 
 def _masks(w, t, direction, state, owner, relf, G):
