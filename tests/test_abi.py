@@ -193,3 +193,27 @@ def test_parity_validation():
               ll.Ext(1, -1, None, None, None, 0.0, 4)):
         assert call(e) == -1
         assert "workspace" in lib.ll_last_error().decode()
+
+
+def test_binding_rejects_host_and_misshapen_tensors():
+    # The binding refuses what the C ABI cannot take before any call: host
+    # tensors, wrong dtypes, non-2-D rows, rows with a non-unit column stride.
+    import pytest
+    import torch
+    rows = torch.zeros((4, 16), dtype=torch.bfloat16)
+    with pytest.raises(ValueError, match="device tensor"):
+        ll.lossy_broadcast(torch.zeros(16), rows, torch.zeros((4, 2), dtype=torch.uint8),
+                           d=16, packet=8)
+    with pytest.raises(ValueError, match="2-D"):
+        ll.lossy_aggregate(torch.zeros(16, dtype=torch.bfloat16), torch.zeros((4, 2), dtype=torch.uint8),
+                           d=16, packet=8, g_hat=torch.zeros(16))
+    with pytest.raises(ValueError, match="unit column stride"):
+        ll.lossy_aggregate(torch.zeros((16, 4), dtype=torch.bfloat16).t(),
+                           torch.zeros((4, 2), dtype=torch.uint8), d=16, packet=8,
+                           g_hat=torch.zeros(16))
+    with pytest.raises(ValueError, match="float32 or bfloat16"):
+        ll.lossy_aggregate(torch.zeros((4, 16), dtype=torch.float16),
+                           torch.zeros((4, 2), dtype=torch.uint8), d=16, packet=8,
+                           g_hat=torch.zeros(16))
+    with pytest.raises(ValueError, match="unknown estimator"):
+        ll.ext(estimator="median")
