@@ -162,3 +162,22 @@ def parity_arrival_probabilities(q: float, group: int, num_packets: int, reliabl
         r = int(rel[lo:hi].sum())  # k itself is not reliable
         out[k] = q + (1.0 - q) * q ** (hi - lo - r)
     return out
+
+
+def ge_arrival_probability(t: int, k, num_packets: int, p_gb: float, p_bg: float,
+                           loss_good: float, loss_bad: float):
+    """Marginal arrival probability of packet k (array-like) of step t under
+    the Gilbert-Elliott process above: the chain starts in Good before step 0
+    and moves once before each packet, so packet k of step t follows
+    n = t * num_packets + k + 1 moves.  For a two-state chain started in Good,
+    P(Bad after n moves) = pi_B (1 - (1 - p_gb - p_bg)^n) with
+    pi_B = p_gb / (p_gb + p_bg) (0 when the chain never moves)."""
+    k = np.asarray(k, dtype=np.float64)
+    n = float(t) * num_packets + k + 1.0
+    s = p_gb + p_bg
+    if s == 0.0:
+        bad = np.zeros_like(n)
+    else:
+        lam = 1.0 - s
+        bad = (p_gb / s) * (1.0 - np.power(lam, n))
+    return 1.0 - (bad * loss_bad + (1.0 - bad) * loss_good)

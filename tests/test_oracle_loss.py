@@ -179,3 +179,31 @@ def test_ge_stationary_loss_and_burst_length():
     mean_run = float(np.mean(runs))
     se = math.sqrt((1 - p_bg) / p_bg**2 / len(runs))
     assert abs(mean_run - 1 / p_bg) < 5 * se, mean_run
+
+
+@pytest.mark.parametrize("p_gb,p_bg,lg,lb", [(0.01, 0.2, 0.0, 0.5), (0.6, 0.7, 0.1, 0.9),
+                                            (0.0, 0.3, 0.05, 0.5), (1.0, 1.0, 0.0, 1.0)])
+def test_ge_marginal_arrival_by_forward_recursion(p_gb, p_bg, lg, lb):
+    # Propagate the state distribution packet by packet with the transition
+    # matrix (no closed form) and compare the marginal arrival probabilities.
+    P = 7
+    T = np.array([[1 - p_gb, p_gb], [p_bg, 1 - p_bg]])
+    dist = np.array([1.0, 0.0])
+    for t in range(3):
+        want = []
+        for k in range(P):
+            dist = dist @ T
+            want.append(1.0 - (dist[0] * lg + dist[1] * lb))
+        got = loss.ge_arrival_probability(t, np.arange(P), P, p_gb, p_bg, lg, lb)
+        assert np.allclose(got, want, atol=1e-14), (t, got, want)
+
+
+def test_ge_marginal_matches_the_drawn_chains():
+    # Empirical arrival rate of the Philox-drawn chains, per packet position,
+    # over many workers: within 5 sigma of the marginal.
+    n, P, p_gb, p_bg, lg, lb = 4000, 12, 0.05, 0.3, 0.0, 0.6
+    a, _ = loss.ge_arrivals(3, 0, loss.GRAD, n, P, p_gb, p_bg, lg, lb, np.zeros(n, np.uint8))
+    q = loss.ge_arrival_probability(0, np.arange(P), P, p_gb, p_bg, lg, lb)
+    rate = a.mean(axis=0)
+    sigma = np.sqrt(q * (1 - q) / n)
+    assert (np.abs(rate - q) < 5 * sigma + 1e-12).all(), (rate, q)
