@@ -153,10 +153,15 @@ typedef struct {
  *                 steps since each replica packet last received the broadcast
  *                 (0 = this step; saturates at 65535).
  *   arrival_prob  q of LL_EST_HORVITZ_THOMPSON in (0, 1].  lossy_aggregate
- *                 requires it; lossy_step_fused takes 0 to mean the arrival
- *                 probability of a Bernoulli gradient loss: q = 1 - p, or with
- *                 parity packets each packet's own q + (1 - q) q^(g - r), g
- *                 the size of its group and r the reliable other members.
+ *                 requires it; lossy_step_fused takes 0 to mean each packet's
+ *                 exact arrival probability under the gradient loss: q = 1 - p
+ *                 for Bernoulli loss, with parity packets q + (1 - q) q^(g - r)
+ *                 (g the size of the packet's group, r its reliable other
+ *                 members); for Gilbert-Elliott loss the chain's marginal
+ *                 1 - (b loss_bad + (1 - b) loss_good) with b = pi_B (1 -
+ *                 (1 - p_gb - p_bg)^n), pi_B = p_gb / (p_gb + p_bg), after
+ *                 n = step * P + k + 1 moves from Good (needs loss_good < 1 and
+ *                 loss_bad < 1).
  *   parity_group  0 (none), or G in [1, 256]: erasure coding over groups of G
  *                 consecutive packets (the parity packets proposed in the
  *                 paper's Section 5).  Per row and group, the sender adds one

@@ -241,6 +241,8 @@ int make_variant(const ExtView& x, double q, const void* g_prev_checked, AggVari
     v->invq = 1.0f;
     v->parity_group = 0;
     v->q = q;
+    v->ge_derived = 0;
+    v->p_gb = v->p_bg = v->loss_good = v->loss_bad = 0.0;
     if (x.est == LL_EST_HORVITZ_THOMPSON) {
         if (!(q > 0.0 && q <= 1.0))
             return fail(LL_EINVAL, "Horvitz-Thompson needs an arrival probability in (0, 1]");
@@ -479,13 +481,28 @@ int lossy_step_fused(int32_t n, int64_t d, int64_t packet, uint64_t step, const 
     if ((r = make_opt(opt, step, m, v, &o))) return r;
     if (x.est == LL_EST_STALE_FILL && (r = check_rows("g_prev", x.g_prev, ld_g, d))) return r;
     double q = x.q;
+    const bool ht_ge = x.est == LL_EST_HORVITZ_THOMPSON && q == 0.0 && ge_g;
     if (x.est == LL_EST_HORVITZ_THOMPSON && q == 0.0) {
-        if (loss_g->kind != LL_LOSS_BERNOULLI)
-            return fail(LL_EINVAL, "Horvitz-Thompson under Gilbert-Elliott loss needs arrival_prob");
-        q = 1.0 - loss_g->p;
+        if (ge_g) {
+            // derived per packet in the kernel; every packet's probability
+            // stays positive when neither state loses everything
+            if (!(loss_g->loss_good < 1.0 && loss_g->loss_bad < 1.0))
+                return fail(LL_EINVAL, "Horvitz-Thompson under Gilbert-Elliott loss with a state "
+                                       "that loses every packet needs arrival_prob");
+            q = 1.0;  // placeholder, replaced per packet
+        } else {
+            q = 1.0 - loss_g->p;
+        }
     }
     AggVariant var;
     if ((r = make_variant(x, q, x.g_prev, &var))) return r;
+    if (ht_ge) {
+        var.ge_derived = 1;
+        var.p_gb = loss_g->p_gb;
+        var.p_bg = loss_g->p_bg;
+        var.loss_good = loss_g->loss_good;
+        var.loss_bad = loss_g->loss_bad;
+    }
     // With parity packets and a derived q, a packet also arrives when it
     // alone was lost in its group and the parity packet came through; the
     // kernel turns q into each packet's probability from its group.

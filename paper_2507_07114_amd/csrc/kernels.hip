@@ -439,6 +439,7 @@ __global__ __launch_bounds__(R::kPacketThreads) void k_step_fused(FusedParams p)
         const bool relp = p.var.reliable != nullptr && p.var.reliable[ch.k] != 0;
         AggVariant var = p.var;
         if (var.parity_group > 0 && !relp) var.invq = parity_invq(var, ch.k, p.P);
+        if (var.ge_derived && !relp) var.invq = ge_invq(var, p.step, ch.k, p.P);
         aggregate8<G>(reinterpret_cast<const typename G::T*>(p.grads), p.ld_g, ch.e0, ch.nv,
                       s_words[0], nw, p.n, K, p.lam, th, var, relp, g);
         update8(p.opt, th, mm, vv, g);

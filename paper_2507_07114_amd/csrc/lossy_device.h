@@ -264,7 +264,23 @@ struct AggVariant {
     // derived per packet: group size (0 = use invq as given) and q.
     int parity_group;
     double q;
+    // Horvitz-Thompson under Gilbert-Elliott loss with the arrival
+    // probability derived per packet from the chain (ge_derived != 0).
+    int ge_derived;
+    double p_gb, p_bg, loss_good, loss_bad;
 };
+
+// 1 / marginal arrival probability of packet k of step t under the
+// Gilbert-Elliott chain: started in Good before step 0 and moved once before
+// each packet, it has made n = t P + k + 1 moves, so P(Bad) = pi_B (1 -
+// (1 - p_gb - p_bg)^n) with pi_B = p_gb / (p_gb + p_bg).
+__device__ __forceinline__ float ge_invq(const AggVariant& v, uint64_t t, int64_t k, int64_t P) {
+    const double n = (double)t * (double)P + (double)k + 1.0;
+    const double s = v.p_gb + v.p_bg;
+    const double bad = s == 0.0 ? 0.0 : (v.p_gb / s) * (1.0 - pow(1.0 - s, n));
+    const double q = 1.0 - (bad * v.loss_bad + (1.0 - bad) * v.loss_good);
+    return (float)(1.0 / q);
+}
 
 // 1 / arrival probability of lossy packet k (of P) of a row under parity
 // packets: it arrives, or it alone was lost in its group of g packets (the

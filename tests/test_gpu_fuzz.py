@@ -67,6 +67,15 @@ CASES += [
          loss=dict(kind=wl.BERNOULLI, p=0.95), est="arrived_mean", owner=-1,
          reliable=False, parity=1, lam=0.1),
 ]
+# Horvitz-Thompson with each packet's probability derived from the chain
+CASES += [
+    dict(case=1003, n=16, packet=1024, d=30_000, gdtype=wl.F32, opt="momentum",
+         loss=dict(kind=wl.GILBERT_ELLIOTT, p_gb=0.05, p_bg=0.3, loss_good=0.02, loss_bad=0.6),
+         est="horvitz_thompson", owner=3, reliable=True, parity=0, lam=0.0),
+    dict(case=1004, n=65, packet=24, d=5_000, gdtype=wl.BF16, opt="adam",
+         loss=dict(kind=wl.GILBERT_ELLIOTT, p_gb=0.7, p_bg=0.6, loss_good=0.1, loss_bad=0.9),
+         est="horvitz_thompson", owner=-1, reliable=False, parity=0, lam=0.0),
+]
 
 
 def _masks(w, t, direction, state, owner, relf, G):
@@ -105,22 +114,29 @@ def test_random_configuration(cfg):
         pi_bad = l["p_gb"] / (l["p_gb"] + l["p_bg"])
         q_lossy = 1 - pi_bad * l["loss_bad"] - (1 - pi_bad) * l["loss_good"]
     prev = torch.zeros_like(dev.grads) if est == "stale_fill" else None
-    # Bernoulli: the fused step derives q (per packet under parity packets);
-    # Gilbert-Elliott: the chain's stationary arrival probability is given.
-    derived = l["kind"] == wl.BERNOULLI
+    # The fused step derives q per packet: Bernoulli 1 - p (per packet under
+    # parity packets), Gilbert-Elliott the chain's marginal at that packet;
+    # a chain state that loses everything needs q given (the stationary one).
+    ge_given = l["kind"] != wl.BERNOULLI and not (l["loss_good"] < 1 and l["loss_bad"] < 1)
     e = ll.ext(estimator=est, owner=owner,
                reliable=None if relf is None else torch.from_numpy(relf).to(DEV),
                g_prev=prev,
-               arrival_prob=q_lossy if (est == "horvitz_thompson" and not derived) else 0.0,
+               arrival_prob=q_lossy if (est == "horvitz_thompson" and ge_given) else 0.0,
                parity_group=G)
-    if derived and G:
-        q = np.tile(oloss.parity_arrival_probabilities(q_lossy, G, P, relf), (w.n, 1))
-    else:
-        q = np.full((w.n, P), q_lossy)
-    if owner >= 0:
-        q[owner] = 1.0
-    if relf is not None:
-        q[:, relf.astype(bool)] = 1.0
+
+    def q_of(t):
+        if l["kind"] == wl.BERNOULLI and G:
+            q = np.tile(oloss.parity_arrival_probabilities(q_lossy, G, P, relf), (w.n, 1))
+        elif l["kind"] == wl.BERNOULLI or ge_given:
+            q = np.full((w.n, P), q_lossy)
+        else:
+            q = np.tile(oloss.ge_arrival_probability(t, np.arange(P), P, l["p_gb"], l["p_bg"],
+                                                     l["loss_good"], l["loss_bad"]), (w.n, 1))
+        if owner >= 0:
+            q[owner] = 1.0
+        if relf is not None:
+            q[:, relf.astype(bool)] = 1.0
+        return q
     packets = list(range(P))
     so = parity.SampledOracle(w, packets, dev)
     prev_o = np.zeros((w.n, w.d), np.uint16 if w.gdtype == wl.BF16 else np.float32)
@@ -138,7 +154,7 @@ def test_random_configuration(cfg):
         orc = ostep.lossy_step(d=w.d, packet=w.packet, packets=packets, gdtype=w.gdtype,
                                grads=g_host, theta=so.theta, m=so.m, v=so.v,
                                replicas=so.replicas, arrived_g=mg, arrived_b=mb, opt=w.opt, t=t,
-                               lam=cfg["lam"], estimator=est, q=q, g_prev=prev_o)
+                               lam=cfg["lam"], estimator=est, q=q_of(t), g_prev=prev_o)
         so.prev_replicas = so.replicas
         so.theta, so.m, so.v, so.replicas = orc["theta"], orc["m"], orc["v"], orc["replicas"]
         parity.compare_step(w, t, dev, so, orc, mb, f"case {cfg['case']} step {t}")
