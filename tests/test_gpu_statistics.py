@@ -104,3 +104,46 @@ def test_worker_lost_for_good():
     R = mb.repeat_interleave(L, dim=1)[:, :d].bool()
     own = theta.to(torch.bfloat16)[None, :].expand(n, -1)
     assert torch.equal(replicas[R].view(torch.int16), own[R].view(torch.int16))
+
+
+def test_horvitz_thompson_under_bursty_loss_is_unbiased_from_the_first_step():
+    # Step 0 of a Gilbert-Elliott chain started in Good, over 20,000 seeds:
+    # with each packet's weight derived from the chain's marginal the fused
+    # step's aggregate (read off an SGD step with lr = 1 from theta = 0) has
+    # expectation mean(g) at every packet, including the first ones where
+    # the chain is far from stationary.
+    from oracle import loss as oloss
+    n, L, P, T = 8, 64, 12, 20_000
+    d = L * P
+    p_gb, p_bg, lg, lb = 0.2, 0.1, 0.0, 0.8
+    rng = np.random.default_rng(4)
+    g = rng.standard_normal((n, d)).astype(np.float32)
+    grads = torch.from_numpy(g).to(DEV)
+    theta = torch.zeros(d, dtype=torch.float32, device=DEV)
+    replicas = torch.zeros((n, d), dtype=torch.float32, device=DEV)
+    ge_g = torch.zeros(n, dtype=torch.uint8, device=DEV)
+    ge_b = torch.zeros(n, dtype=torch.uint8, device=DEV)
+    ws = torch.zeros(ll.ll_workspace_bytes(n, d, L), dtype=torch.uint8, device=DEV)
+    acc = torch.zeros(d, dtype=torch.float64, device=DEV)
+    e = ll.ext(estimator="horvitz_thompson")  # arrival_prob 0: derived per packet
+    opt = ll.sgd(1.0)
+    print(f"bursty-loss Horvitz-Thompson: {T} seeds", flush=True)
+    for s in range(T):
+        theta.zero_()
+        ge_g.zero_()
+        ge_b.zero_()
+        spec = ll.gilbert_elliott(p_gb, p_bg, lg, lb, seed=s + 1)
+        ll.lossy_step_fused(d=d, packet=L, step=0, loss_g=spec, loss_b=spec, grads=grads, opt=opt,
+                            theta=theta, replicas=replicas, ge_state_g=ge_g, ge_state_b=ge_b,
+                            workspace=ws, ext=e)
+        acc -= theta.double()
+    mc = (acc / T).cpu().numpy()
+    q = oloss.ge_arrival_probability(0, np.arange(P), P, p_gb, p_bg, lg, lb)   # [P]
+    Q = np.repeat(q, L)
+    g64 = g.astype(np.float64)
+    var = (g64 ** 2 * ((1 - Q) / Q)[None, :]).sum(axis=0) / n**2
+    err = np.abs(mc - g64.mean(axis=0))
+    assert (err <= 5.5 * np.sqrt(var / T) + 1e-9).all(), float((err / np.sqrt(var / T)).max())
+    # the stationary weight would have been visibly biased on the first packet
+    q_stat = 1 - (p_gb / (p_gb + p_bg)) * lb
+    assert abs(q[0] - q_stat) > 0.3
