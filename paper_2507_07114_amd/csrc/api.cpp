@@ -251,6 +251,38 @@ int make_variant(const ExtView& x, double q, const void* g_prev_checked, AggVari
     return LL_OK;
 }
 
+// Aggregation variant of the fused step.  An explicit Horvitz-Thompson
+// arrival_prob is used as given; 0 asks for each packet's exact arrival
+// probability under the gradient loss, derived in the kernel: 1 - p for
+// Bernoulli loss, turned per packet into q + (1 - q) q^(g - r) under parity
+// packets (a packet also arrives when it alone was lost in its group and the
+// parity packet came through), and the chain's marginal at the packet under
+// Gilbert-Elliott loss (positive only if neither state loses everything).
+int fused_variant(const ExtView& x, const ll_loss* loss_g, AggVariant* var) {
+    const bool derive = x.est == LL_EST_HORVITZ_THOMPSON && x.q == 0.0;
+    const bool ge = loss_g->kind == LL_LOSS_GILBERT_ELLIOTT;
+    double q = x.q;
+    if (derive && ge) {
+        if (!(loss_g->loss_good < 1.0 && loss_g->loss_bad < 1.0))
+            return fail(LL_EINVAL, "Horvitz-Thompson under Gilbert-Elliott loss with a state "
+                                   "that loses every packet needs arrival_prob");
+        q = 1.0;  // replaced per packet
+    } else if (derive) {
+        q = 1.0 - loss_g->p;
+    }
+    int r = make_variant(x, q, x.g_prev, var);
+    if (r) return r;
+    if (derive && ge) {
+        var->ge_derived = 1;
+        var->p_gb = loss_g->p_gb;
+        var->p_bg = loss_g->p_bg;
+        var->loss_good = loss_g->loss_good;
+        var->loss_bad = loss_g->loss_bad;
+    }
+    if (derive && x.parity) var->parity_group = x.parity;
+    return LL_OK;
+}
+
 // Fill one direction's Gilbert-Elliott job with its scratch carved from `base`.
 GeJob make_ge_job(const ll_loss* l, int dir, uint8_t* state, uint8_t* arrived,
                   const GeScratch& gs, uint8_t* base) {
@@ -480,33 +512,8 @@ int lossy_step_fused(int32_t n, int64_t d, int64_t packet, uint64_t step, const 
     OptParams o;
     if ((r = make_opt(opt, step, m, v, &o))) return r;
     if (x.est == LL_EST_STALE_FILL && (r = check_rows("g_prev", x.g_prev, ld_g, d))) return r;
-    double q = x.q;
-    const bool ht_ge = x.est == LL_EST_HORVITZ_THOMPSON && q == 0.0 && ge_g;
-    if (x.est == LL_EST_HORVITZ_THOMPSON && q == 0.0) {
-        if (ge_g) {
-            // derived per packet in the kernel; every packet's probability
-            // stays positive when neither state loses everything
-            if (!(loss_g->loss_good < 1.0 && loss_g->loss_bad < 1.0))
-                return fail(LL_EINVAL, "Horvitz-Thompson under Gilbert-Elliott loss with a state "
-                                       "that loses every packet needs arrival_prob");
-            q = 1.0;  // placeholder, replaced per packet
-        } else {
-            q = 1.0 - loss_g->p;
-        }
-    }
     AggVariant var;
-    if ((r = make_variant(x, q, x.g_prev, &var))) return r;
-    if (ht_ge) {
-        var.ge_derived = 1;
-        var.p_gb = loss_g->p_gb;
-        var.p_bg = loss_g->p_bg;
-        var.loss_good = loss_g->loss_good;
-        var.loss_bad = loss_g->loss_bad;
-    }
-    // With parity packets and a derived q, a packet also arrives when it
-    // alone was lost in its group and the parity packet came through; the
-    // kernel turns q into each packet's probability from its group.
-    if (x.est == LL_EST_HORVITZ_THOMPSON && x.q == 0.0 && x.parity) var.parity_group = x.parity;
+    if ((r = fused_variant(x, loss_g, &var))) return r;
     const WsLayout w = ws_layout(n, g);
     const bool need_ws = drift || ge_g || ge_b || x.parity;
     if (need_ws) {
