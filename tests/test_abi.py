@@ -217,3 +217,14 @@ def test_binding_rejects_host_and_misshapen_tensors():
                            g_hat=torch.zeros(16))
     with pytest.raises(ValueError, match="unknown estimator"):
         ll.ext(estimator="median")
+
+
+def test_missing_library_fails_loudly(monkeypatch):
+    # No fallback: without liblossy.so every entry point raises.
+    import pytest
+    monkeypatch.setattr(ll, "_lib", None)
+    monkeypatch.setattr(ll, "library_path", lambda: "/nonexistent/liblossy.so")
+    with pytest.raises(RuntimeError, match="not built"):
+        ll.ll_workspace_bytes(4, 100, 8)
+    with pytest.raises(RuntimeError, match="not built"):
+        ll.ll_last_error()
