@@ -1,7 +1,7 @@
 """Shared helpers of the GPU parity tests: host copies of sampled packets and
 the comparison norms.
 
-Norms (the floating-point reasoning behind each is in the design notes):
+Norms, each with the floating-point reasoning behind it:
   * masks, counts, packet bookkeeping, GE state: bit-exact.
   * g_hat: |gpu - orc| <= max(1e-5, K 2^-24) * A_e, A_e = mean |arrived
     contribution| (for an empty packet A_e = |lam * theta|).  A sequential
