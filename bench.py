@@ -252,9 +252,13 @@ def main():
             rel_np = np.zeros(w.num_packets, np.uint8)
             rel_np[:: args.reliable_every] = 1
             rel_t = torch.from_numpy(rel_np).cuda()
+        # Horvitz-Thompson weights are derived per packet by the library
+        # (arrival_prob 0), except for a chain with a state that loses every
+        # packet, where the stationary arrival probability is given.
         q = 0.0
-        if args.estimator == "horvitz_thompson" and w.loss["kind"] != wl.BERNOULLI:
-            l = w.loss
+        l = w.loss
+        if (args.estimator == "horvitz_thompson" and l["kind"] != wl.BERNOULLI
+                and not (l["loss_good"] < 1 and l["loss_bad"] < 1)):
             pi_bad = l["p_gb"] / (l["p_gb"] + l["p_bg"])
             q = 1 - pi_bad * l["loss_bad"] - (1 - pi_bad) * l["loss_good"]
         ext = ll.ext(estimator=args.estimator, owner=args.owner, reliable=rel_t,
