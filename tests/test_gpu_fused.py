@@ -1,7 +1,6 @@
 """The fused step: bit-identical to the stage-by-stage chain, parity with the
 oracle on scaled-down workloads (several tiles and a ragged tail), edge
 cases, determinism and exact resume."""
-import math
 
 import numpy as np
 import pytest
