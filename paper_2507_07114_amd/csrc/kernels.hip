@@ -119,7 +119,7 @@ __device__ __forceinline__ uint32_t ge_packet_map(uint64_t u0, const GeParams& g
 __device__ __forceinline__ void ge_block_scan(uint32_t* s) {
     for (int off = 1; off < kThreads; off <<= 1) {
         const uint32_t mine = s[threadIdx.x];
-        const uint32_t before = threadIdx.x >= off ? s[threadIdx.x - off] : kGeIdentity;
+        const uint32_t before = (int)threadIdx.x >= off ? s[threadIdx.x - off] : kGeIdentity;
         __syncthreads();
         s[threadIdx.x] = ge_compose(mine, before);
         __syncthreads();
@@ -343,7 +343,7 @@ __device__ __forceinline__ DriftAcc block_fold(DriftAcc a) {
     s_acc[threadIdx.x] = a;
     __syncthreads();
     for (int off = kThreads / 2; off > 0; off >>= 1) {
-        if (threadIdx.x < off) s_acc[threadIdx.x].add(s_acc[threadIdx.x + off]);
+        if ((int)threadIdx.x < off) s_acc[threadIdx.x].add(s_acc[threadIdx.x + off]);
         __syncthreads();
     }
     return s_acc[0];
