@@ -24,7 +24,7 @@ ARCH = "gfx950"
 # -packed-fp32-ops: keep the compiler from emitting packed fp32 VALU forms.
 COMMON = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-fvisibility=hidden",
-    "-ffp-contract=off", "-Wall", "-Wno-unused-result",
+    "-ffp-contract=off", "-Wall", "-Wextra", "-Wno-unused-result",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
     f"-I{INCLUDE}", f"-I{CSRC}",
 ]
