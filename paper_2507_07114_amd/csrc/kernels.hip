@@ -369,6 +369,22 @@ __global__ __launch_bounds__(kThreads) void k_drift_reduce(const DriftPartial* p
     if (threadIdx.x == 0) out[blockIdx.x] = t;
 }
 
+// The ll_drift record from the folded totals (thread 0 of the caller).
+__device__ __forceinline__ void write_drift(const DriftAcc& t, int n, int64_t d, int have_master,
+                                            DriftOut* out) {
+    const double pairs = (double)n * (double)(n - 1) * 0.5;
+    const double denom = (double)d * pairs;
+    DriftOut r;
+    r.max_abs = t.range;
+    r.mean_sq = denom > 0.0 ? t.pair / denom : 0.0;
+    r.rms = sqrt(r.mean_sq);
+    r.mean_abs_to_master =
+        have_master ? (d > 0 ? t.abs_sum / ((double)n * (double)d) : 0.0) : (double)NAN;
+    r.stale_packets = t.stale;
+    r.empty_packets = t.empty;
+    *out = r;
+}
+
 __global__ __launch_bounds__(kThreads) void k_drift_final(const DriftAcc* groups, int n,
                                                           int64_t d, int have_master,
                                                           DriftOut* out) {
@@ -376,24 +392,31 @@ __global__ __launch_bounds__(kThreads) void k_drift_final(const DriftAcc* groups
     a.zero();
     for (int j = threadIdx.x; j < kReduceGroups; j += kThreads) a.add(groups[j]);
     const DriftAcc t = block_fold(a);
-    if (threadIdx.x == 0) {
-        const double pairs = (double)n * (double)(n - 1) * 0.5;
-        const double denom = (double)d * pairs;
-        DriftOut r;
-        r.max_abs = t.range;
-        r.mean_sq = denom > 0.0 ? t.pair / denom : 0.0;
-        r.rms = sqrt(r.mean_sq);
-        r.mean_abs_to_master =
-            have_master ? (d > 0 ? t.abs_sum / ((double)n * (double)d) : 0.0) : (double)NAN;
-        r.stale_packets = t.stale;
-        r.empty_packets = t.empty;
-        *out = r;
-    }
+    if (threadIdx.x == 0) write_drift(t, n, d, have_master, out);
+}
+
+// Few partials (small shards): one workgroup folds them directly, in a fixed
+// order, saving the second launch.
+constexpr int64_t kDirectFold = 2048;
+
+__global__ __launch_bounds__(kThreads) void k_drift_direct(const DriftPartial* parts, int64_t count,
+                                                           int n, int64_t d, int have_master,
+                                                           DriftOut* out) {
+    DriftAcc a;
+    a.zero();
+    for (int64_t j = threadIdx.x; j < count; j += kThreads) a.add(parts[j]);
+    const DriftAcc t = block_fold(a);
+    if (threadIdx.x == 0) write_drift(t, n, d, have_master, out);
 }
 
 static hipError_t launch_drift_reduce(const DriftPartial* parts, int64_t count, DriftAcc* groups,
                                       int n, int64_t d, int have_master, DriftOut* out,
                                       hipStream_t s) {
+    if (count <= kDirectFold) {
+        hipLaunchKernelGGL(k_drift_direct, dim3(1), dim3(kThreads), 0, s, parts, count, n, d,
+                           have_master, out);
+        return hipGetLastError();
+    }
     hipLaunchKernelGGL(k_drift_reduce, dim3(kReduceGroups), dim3(kThreads), 0, s, parts, count,
                        groups);
     hipError_t e = hipGetLastError();
