@@ -276,17 +276,20 @@ LL_API int drift_stats(int32_t n, int64_t d, int64_t packet, int32_t rdtype,
  *   ll_masks(GRAD) -> lossy_aggregate -> shard_step -> ll_masks(BCAST)
  *   -> lossy_broadcast -> drift_stats
  * (and ll_ages_update) with the same arithmetic, so its outputs are
- * bit-identical to that chain.
+ * bit-identical to that chain given the same ext (except Horvitz-Thompson
+ * weights derived per packet, arrival_prob = 0 under parity packets or
+ * Gilbert-Elliott loss, which lossy_aggregate cannot take).
  *   loss_g, loss_b, opt     host structs.
  *   ge_state_g, ge_state_b  uint8 [n] each (device, in/out) for
  *                           Gilbert-Elliott processes, else may be NULL.
  *   arrived_g, arrived_b    uint8 [n][P] (out, may be NULL): the masks drawn.
  *   counts                  int32 [P] (out, may be NULL): gradient arrivals.
  *   workspace, ws_bytes     scratch, ws_bytes >= ll_workspace_bytes(n, d, packet);
- *                           required with drift or a Gilbert-Elliott process.
+ *                           required with drift, a Gilbert-Elliott process or
+ *                           parity packets.
  *   drift                   ll_drift (device, out) or NULL to skip drift.
  *   ext                     NULL, or variants (estimator, owner, reliable,
- *                           g_prev, ages).
+ *                           g_prev, ages, parity_group).
  * Lost gradient packets are never read; lost broadcast packets are read only
  * for drift and never written.
  */
