@@ -176,3 +176,48 @@ def test_drift_stays_bounded_over_two_thousand_steps():
     for r in windows[1:]:   # the first window includes the burn-in from identical replicas
         assert abs(r - corrected) < 0.04 * corrected
     assert max(windows[1:]) - min(windows[1:]) < 0.04 * corrected
+
+
+def test_full_size_variants_on_the_7b_shard():
+    # The 7B-shard workload at full size with every delivery variant at once:
+    # owner row, every 10th packet reliable, parity packets in groups of 7
+    # (the last group ragged: 25,696 = 7 * 3670 + 6), Horvitz-Thompson with
+    # each packet's weight derived in the kernel, broadcast ages.
+    from oracle import loss as oloss
+    from oracle import step as ostep
+    w = wl.WORKLOADS["n64_llama7b_shard_bf16_adam"]
+    P, G, owner, p = w.num_packets, 7, 5, w.loss["p"]
+    assert P % G != 0
+    relf = np.zeros(P, np.uint8)
+    relf[::10] = 1
+    dev = parity.DeviceState(w)
+    ages = torch.zeros((w.n, P), dtype=torch.int16, device=DEV)
+    e = ll.ext(estimator="horvitz_thompson", owner=owner,
+               reliable=torch.from_numpy(relf).to(DEV), ages=ages, parity_group=G)
+    packets = sorted(set(wl.packet_sample(w, 20)) | {P - 6, P - 1, 10, 11})
+    so = parity.SampledOracle(w, packets, dev)
+    try:
+        g_host = parity.host_rows(dev.grads, so.idx, w.gdtype)
+        dev.fused(0, ext=e)
+
+        def masks(direction):
+            a = oloss.apply_overrides(
+                oloss.bernoulli_arrivals(w.seed, 0, direction, w.n, np.arange(P), p), owner, relf)
+            par = oloss.parity_arrivals(w.seed, 0, direction, w.n, np.arange((P + G - 1) // G), p)
+            return oloss.parity_recover(a, G, par)
+        mg, mb = masks(0), masks(1)
+        assert np.array_equal(dev.arrived_g.cpu().numpy(), mg)
+        assert np.array_equal(dev.arrived_b.cpu().numpy(), mb)
+        assert np.array_equal(ages.cpu().numpy().view(np.uint16), np.where(mb == 1, 0, 1))
+        q = np.tile(oloss.parity_arrival_probabilities(1 - p, G, P, relf), (w.n, 1))
+        q[owner] = 1.0
+        orc = ostep.lossy_step(d=w.d, packet=w.packet, packets=packets, gdtype=w.gdtype,
+                               grads=g_host, theta=so.theta, m=so.m, v=so.v,
+                               replicas=so.replicas, arrived_g=mg[:, packets],
+                               arrived_b=mb[:, packets], opt=w.opt, t=0,
+                               estimator="horvitz_thompson", q=q[:, packets])
+        so.prev_replicas = so.replicas
+        parity.compare_step(w, 0, dev, so, orc, mb[:, packets], "7B shard, all variants")
+    finally:
+        del dev
+        _free()
