@@ -285,7 +285,7 @@ def main():
     ge_ws = torch.zeros(max(ll.ll_masks_workspace_bytes(w.n, P), 256), dtype=torch.uint8,
                         device="cuda")
     per_step_bytes = []
-    mext = None if ext is None else ll.ext(owner=args.owner, reliable=ext._tensors[0],
+    mext = None if ext is None else ll.ext(owner=args.owner, reliable=ext.reliable,
                                            parity_group=args.parity_group)
     for t in range(args.warmup + args.steps):
         ll.ll_masks(w.n, P, t, ll.LL_DIR_GRAD, spec, mg_dev, ge_state=ge_g, workspace=ge_ws,

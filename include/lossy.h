@@ -27,15 +27,21 @@
  *     without synchronising; device outputs are valid once the stream has
  *     reached that point.  Calls can therefore be captured into a HIP graph;
  *     a replay repeats the captured step index.
- *   - Row-major [N][ld] buffers: row i starts at element i * ld.  ld >= D.
+ *   - Row-major [N][ld] buffers: row i starts at element i * ld.  ld >= D and
+ *     ld times the element size (4 bytes fp32, 2 bytes bf16) is a multiple of
+ *     16 bytes, so every row starts on a 16-byte boundary.
+ *   - Any packet length L >= 1 is accepted.  Packets whose start is a multiple
+ *     of 8 elements (L a multiple of 8) are moved with 16-byte vector accesses;
+ *     other packets, and the last 1..7 elements of a shard whose D is not a
+ *     multiple of 8, are moved element by element (same results, slower).
  *   - Masks are uint8 [N][P] (row i = worker/replica i, column k = packet),
  *     1 = arrived, 0 = lost.
  *   - Return codes: LL_OK (0); LL_EINVAL (-1) for a bad size or argument
- *     (N outside [1, 1024], D < 0, L < 8 or L not a multiple of 8, ld < D,
+ *     (N outside [1, 1024], D < 0, L < 1, ld < D,
  *     a probability outside [0, 1], an unknown kind or dtype, a required
  *     pointer that is NULL, a workspace that is too small, or a launch that
  *     would exceed the grid limit); LL_EALIGN (-2) when a buffer address is
- *     not 16-byte aligned or ld is not a multiple of 8 elements; LL_EHIP
+ *     not 16-byte aligned or ld * element size is not a multiple of 16; LL_EHIP
  *     (-3) when the HIP runtime reports an error.  ll_last_error() then
  *     returns a message (thread-local, valid until the next call on that
  *     thread).  No exception crosses this boundary.
@@ -302,6 +308,67 @@ LL_API int lossy_step_fused(int32_t n, int64_t d, int64_t packet, uint64_t step,
                      uint8_t* arrived_g, uint8_t* arrived_b, int32_t* counts,
                      void* workspace, size_t ws_bytes, ll_drift* drift,
                      const ll_ext* ext, void* stream);
+
+/*
+ * Pacing of lossy_step_fused (a performance setting of this library, not part
+ * of the paper's method; it never changes a result).  The fused step streams
+ * all N gradient rows and all N replica rows of every packet.  When each
+ * workgroup walks the rows on its own, the chip has pieces of every row in
+ * flight at once and the HBM serves them well below its streaming rate.  A
+ * paced step gives each workgroup one tile (a chunk of a packet, 4 KiB of
+ * every row) as before, but groups the tiles into rounds of adjacent tiles;
+ * in each round's sweeps (gradient rows, replica rows, stale replica rows
+ * read for drift) the access of row i waits for a slot time on the 100 MHz
+ * clock that all compute units share, so the chip streams a few long runs of
+ * one row at a time.  A slot lasts as long as its expected bytes take at the
+ * round's share of bytes_per_s; a round starts with a lead (the workgroups
+ * start and read their master and moments) and has a gap between its
+ * gradient and replica sweeps (the update).  Laid out too fast, the schedule
+ * is not kept and the speed falls back towards the unpaced one; too slow, the
+ * step runs at the set rate.
+ *   mode         LL_PACE_AUTO (default): paced when the step spans at least 8
+ *                rounds; LL_PACE_ALWAYS; LL_PACE_NEVER.
+ *   bytes_per_s  rate the slots are laid out for (default 6.0e12).
+ *   gap_us       time between the last gradient slot and the first replica
+ *                slot, besides the master and moment writes (default 2).
+ *   lead_us      time from a round's start to its first gradient slot,
+ *                besides the master and moment reads (default 2.5).
+ *   overlap      rounds streaming at once (1 or 2; default 2): with 2, each
+ *                round gets half the rate and rounds start half a round
+ *                apart, so one round's gradient sweep runs beside the
+ *                previous round's replica sweep and each round's lead and gap
+ *                are covered by the other's streams.
+ *   resident     rounds sharing the workgroup places the chip holds at once
+ *                (overlap..4; default 2): a round has headroom / resident of
+ *                them, and rounds start no closer than a round's length /
+ *                resident apart, so that every round's workgroups find places
+ *                when it starts.
+ *   headroom     fraction of those places the rounds fill ((0, 1]; 0.9).
+ * The setting is process-wide and read at each call.  A paced step enqueues,
+ * before the step itself: the Bernoulli mask kernel for each direction whose
+ * masks have memory to go to (the caller's mask output, else the workspace
+ * when one of ll_workspace_bytes() bytes is passed), so that the step reads
+ * its masks instead of drawing them at the start of every round; and a
+ * one-lane kernel that stores the schedule's start time in a per-device
+ * device variable.  Overlapping paced steps on one device can read each
+ * other's start time, which costs speed but changes no result.
+ * ll_set_pacing returns LL_EINVAL for an unknown mode or a field outside the
+ * ranges above (bytes_per_s in (0, 1e15), gap_us and lead_us in [0, 1e4]);
+ * ll_get_pacing fills `out` (host).
+ */
+enum { LL_PACE_AUTO = 0, LL_PACE_ALWAYS = 1, LL_PACE_NEVER = 2 };
+typedef struct {
+    int32_t mode;
+    double bytes_per_s;
+    double gap_us;
+    double lead_us;
+    int32_t overlap;
+    int32_t resident;
+    double headroom;
+} ll_pacing;
+
+LL_API int ll_set_pacing(const ll_pacing* cfg);
+LL_API int ll_get_pacing(ll_pacing* out);
 
 /* Bytes of device workspace that drift_stats and lossy_step_fused need for
  * these sizes (0 on invalid sizes): drift partials, two mask areas and the

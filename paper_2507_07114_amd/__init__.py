@@ -20,9 +20,9 @@ __all__ = [
     # entry points of include/lossy.h
     "ll_masks", "ll_ages_update", "lossy_aggregate", "shard_step", "lossy_broadcast",
     "drift_stats", "lossy_step_fused", "ll_workspace_bytes", "ll_masks_workspace_bytes",
-    "ll_last_error",
+    "ll_last_error", "ll_set_pacing", "ll_get_pacing",
     # argument structs and their builders
-    "LossSpec", "OptSpec", "Ext", "bernoulli", "gilbert_elliott", "sgd", "sgd_momentum", "adam",
+    "LossSpec", "OptSpec", "Ext", "ExtArgs", "Pacing", "bernoulli", "gilbert_elliott", "sgd", "sgd_momentum", "adam",
     "ext", "ESTIMATORS",
     # helpers
     "drift_buffer", "read_drift", "library_path", "LossyError",
@@ -72,21 +72,90 @@ class Ext(ctypes.Structure):
                 ("parity_group", ctypes.c_int32)]
 
 
+class ExtArgs:
+    """Variants of the step as tensors and numbers (see ext()); turned into
+    an ll_ext only when a call has checked them against its other arguments."""
+
+    def __init__(self, estimator: int, owner: int, reliable, g_prev, ages, arrival_prob: float,
+                 parity_group: int):
+        self.estimator = estimator
+        self.owner = owner
+        self.reliable = reliable
+        self.g_prev = g_prev
+        self.ages = ages
+        self.arrival_prob = arrival_prob
+        self.parity_group = parity_group
+
+    def check(self, n: int, num_packets: int, grads: Optional[torch.Tensor]):
+        if self.reliable is not None:
+            _need_numel(self.reliable, "reliable", num_packets, torch.uint8)
+        if self.ages is not None:
+            _need_shape(self.ages, "ages", (n, num_packets), torch.int16)
+        if self.g_prev is not None and grads is not None:
+            g = self.g_prev
+            if (g.dim() != 2 or tuple(g.shape) != tuple(grads.shape) or g.dtype != grads.dtype
+                    or (g.numel() and g.stride() != grads.stride())):
+                raise ValueError(
+                    f"g_prev must match grads in shape, row stride and dtype: got "
+                    f"{tuple(g.shape)} stride {g.stride()} {g.dtype}, grads "
+                    f"{tuple(grads.shape)} stride {grads.stride()} {grads.dtype}")
+
+    def as_struct(self) -> "Ext":
+        e = Ext(self.estimator, self.owner, _flat(self.reliable, "reliable", torch.uint8),
+                None if self.g_prev is None else _rows(self.g_prev, "g_prev")[0],
+                _flat(self.ages, "ages", torch.int16), self.arrival_prob, self.parity_group)
+        e._tensors = (self.reliable, self.g_prev, self.ages)  # pointers stay valid while e lives
+        return e
+
+
 def ext(estimator: str = "arrived_mean", owner: int = -1,
         reliable: Optional[torch.Tensor] = None, g_prev: Optional[torch.Tensor] = None,
         ages: Optional[torch.Tensor] = None, arrival_prob: float = 0.0,
-        parity_group: int = 0) -> Ext:
+        parity_group: int = 0) -> ExtArgs:
     if estimator not in ESTIMATORS:
         raise ValueError(f"unknown estimator {estimator!r}")
-    e = Ext(ESTIMATORS[estimator], owner, _flat(reliable, "reliable", torch.uint8),
-            None if g_prev is None else _rows(g_prev, "g_prev")[0],
-            _flat(ages, "ages", torch.int16), arrival_prob, parity_group)
-    e._tensors = (reliable, g_prev, ages)  # the pointers above stay valid while e lives
-    return e
+    return ExtArgs(ESTIMATORS[estimator], owner, reliable, g_prev, ages, arrival_prob,
+                   parity_group)
 
 
-def _ext_ref(e: Optional[Ext]):
-    return None if e is None else ctypes.byref(e)
+def _ext_ref(e, n: int = 0, num_packets: int = 0, grads: Optional[torch.Tensor] = None):
+    """ll_ext* for a call: None, a raw Ext as given, or an ExtArgs checked
+    against the call's sizes and then marshalled."""
+    if e is None:
+        return None
+    if isinstance(e, ExtArgs):
+        e.check(n, num_packets, grads)
+        e = e.as_struct()
+    return ctypes.byref(e)
+
+
+def _num_packets(d: int, packet: int) -> int:
+    return (d + packet - 1) // packet if packet >= 1 and d >= 0 else 0
+
+
+def _need_numel(t: Optional[torch.Tensor], name: str, numel: int, dtype=None):
+    if t is None:
+        return
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name} must have dtype {dtype}, got {t.dtype}")
+    if t.numel() < numel:
+        raise ValueError(f"{name} has {t.numel()} elements, needs at least {numel}")
+
+
+def _need_shape(t: Optional[torch.Tensor], name: str, shape, dtype=None):
+    if t is None:
+        return
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name} must have dtype {dtype}, got {t.dtype}")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+
+
+def _need_rows(t: torch.Tensor, name: str, d: int):
+    if t.dim() != 2:
+        raise ValueError(f"{name} must be 2-D")
+    if t.shape[1] < d:
+        raise ValueError(f"{name} rows hold {t.shape[1]} elements, fewer than d={d}")
 
 
 def bernoulli(p: float, seed: int = 0) -> LossSpec:
@@ -132,6 +201,8 @@ _SIGNATURES = {
                                         ctypes.POINTER(Ext), _vp]),
     "ll_workspace_bytes": (ctypes.c_size_t, [_i32, _i64, _i64]),
     "ll_last_error": (ctypes.c_char_p, []),
+    "ll_set_pacing": (ctypes.c_int, [ctypes.c_void_p]),
+    "ll_get_pacing": (ctypes.c_int, [ctypes.c_void_p]),
 }
 
 
@@ -149,6 +220,35 @@ def _load():
             fn.argtypes = args
         _lib = lib
     return _lib
+
+
+class Pacing(ctypes.Structure):
+    _fields_ = [("mode", ctypes.c_int32), ("bytes_per_s", ctypes.c_double),
+                ("gap_us", ctypes.c_double), ("lead_us", ctypes.c_double),
+                ("overlap", ctypes.c_int32), ("resident", ctypes.c_int32),
+                ("headroom", ctypes.c_double)]
+
+
+PACE_MODES = {"auto": 0, "always": 1, "never": 2}
+
+
+def ll_set_pacing(mode: str = "auto", bytes_per_s: float = 6.0e12, gap_us: float = 2.0,
+                  lead_us: float = 2.5, overlap: int = 2, resident: int = 2,
+                  headroom: float = 0.9) -> None:
+    """Process-wide pacing of lossy_step_fused (a performance setting; see
+    include/lossy.h)."""
+    if mode not in PACE_MODES:
+        raise ValueError(f"unknown pacing mode {mode!r}")
+    cfg = Pacing(PACE_MODES[mode], bytes_per_s, gap_us, lead_us, overlap, resident, headroom)
+    _check("ll_set_pacing", _load().ll_set_pacing(ctypes.byref(cfg)))
+
+
+def ll_get_pacing() -> dict:
+    cfg = Pacing()
+    _check("ll_get_pacing", _load().ll_get_pacing(ctypes.byref(cfg)))
+    mode = {v: k for k, v in PACE_MODES.items()}[cfg.mode]
+    return dict(mode=mode, bytes_per_s=cfg.bytes_per_s, gap_us=cfg.gap_us, lead_us=cfg.lead_us,
+                overlap=cfg.overlap, resident=cfg.resident, headroom=cfg.headroom)
 
 
 def ll_last_error() -> str:
@@ -203,17 +303,21 @@ def _flat(t: Optional[torch.Tensor], name: str, dtype) -> Optional[int]:
 
 def ll_masks(n: int, num_packets: int, step: int, direction: int, loss: LossSpec,
              arrived: torch.Tensor, ge_state: Optional[torch.Tensor] = None,
-             workspace: Optional[torch.Tensor] = None, ext: Optional[Ext] = None) -> None:
+             workspace: Optional[torch.Tensor] = None, ext=None) -> None:
+    _need_shape(arrived, "arrived", (n, num_packets), torch.uint8)
+    _need_numel(ge_state, "ge_state", n, torch.uint8)
+    ref = _ext_ref(ext, n, num_packets)
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     _check("ll_masks", _load().ll_masks(
         n, num_packets, step, direction, ctypes.byref(loss),
         _flat(ge_state, "ge_state", torch.uint8), _flat(arrived, "arrived", torch.uint8),
-        _dev(workspace, "workspace"), ws_bytes, _ext_ref(ext), _stream()))
+        _dev(workspace, "workspace"), ws_bytes, ref, _stream()))
 
 
 def ll_ages_update(arrived_bc: torch.Tensor, ages: torch.Tensor) -> None:
     """ages (int16 storage of uint16 counts) [n][P] after a broadcast."""
     n, P = arrived_bc.shape
+    _need_shape(ages, "ages", (n, P), torch.int16)
     _check("ll_ages_update", _load().ll_ages_update(
         n, P, _flat(arrived_bc, "arrived_bc", torch.uint8), _flat(ages, "ages", torch.int16),
         _stream()))
@@ -226,19 +330,28 @@ def ll_masks_workspace_bytes(n: int, num_packets: int) -> int:
 def lossy_aggregate(grads: torch.Tensor, arrived: torch.Tensor, *, d: int, packet: int,
                     g_hat: torch.Tensor, fallback_lambda: float = 0.0,
                     theta: Optional[torch.Tensor] = None,
-                    counts: Optional[torch.Tensor] = None, ext: Optional[Ext] = None) -> None:
+                    counts: Optional[torch.Tensor] = None, ext=None) -> None:
+    _need_rows(grads, "grads", d)
+    n, P = grads.shape[0], _num_packets(d, packet)
+    _need_shape(arrived, "arrived", (n, P), torch.uint8)
+    _need_numel(g_hat, "g_hat", d, torch.float32)
+    _need_numel(theta, "theta", d, torch.float32)
+    _need_numel(counts, "counts", P, torch.int32)
+    ref = _ext_ref(ext, n, P, grads)
     gp, ld, gt = _rows(grads, "grads")
     _check("lossy_aggregate", _load().lossy_aggregate(
-        grads.shape[0], d, packet, gt, gp, ld, _flat(arrived, "arrived", torch.uint8),
+        n, d, packet, gt, gp, ld, _flat(arrived, "arrived", torch.uint8),
         fallback_lambda, _flat(theta, "theta", torch.float32),
         _flat(g_hat, "g_hat", torch.float32), _flat(counts, "counts", torch.int32),
-        _ext_ref(ext), _stream()))
+        ref, _stream()))
 
 
 def shard_step(opt: OptSpec, step: int, theta: torch.Tensor, g_hat: torch.Tensor,
                m: Optional[torch.Tensor] = None, v: Optional[torch.Tensor] = None,
                d: Optional[int] = None) -> None:
     d = theta.numel() if d is None else d
+    for t, name in ((theta, "theta"), (g_hat, "g_hat"), (m, "m"), (v, "v")):
+        _need_numel(t, name, d, torch.float32)
     _check("shard_step", _load().shard_step(
         ctypes.byref(opt), d, step, _flat(theta, "theta", torch.float32),
         _flat(m, "m", torch.float32), _flat(v, "v", torch.float32),
@@ -247,6 +360,10 @@ def shard_step(opt: OptSpec, step: int, theta: torch.Tensor, g_hat: torch.Tensor
 
 def lossy_broadcast(theta: torch.Tensor, replicas: torch.Tensor, arrived_bc: torch.Tensor, *,
                     d: int, packet: int) -> None:
+    _need_rows(replicas, "replicas", d)
+    _need_numel(theta, "theta", d, torch.float32)
+    _need_shape(arrived_bc, "arrived_bc", (replicas.shape[0], _num_packets(d, packet)),
+                torch.uint8)
     rp, ld, rt = _rows(replicas, "replicas")
     _check("lossy_broadcast", _load().lossy_broadcast(
         replicas.shape[0], d, packet, _flat(theta, "theta", torch.float32), rt, rp, ld,
@@ -270,6 +387,11 @@ def read_drift(buf: torch.Tensor) -> dict:
 def drift_stats(replicas: torch.Tensor, *, d: int, packet: int, workspace: torch.Tensor,
                 out: torch.Tensor, theta: Optional[torch.Tensor] = None,
                 arrived_bc: Optional[torch.Tensor] = None) -> None:
+    _need_rows(replicas, "replicas", d)
+    _need_numel(theta, "theta", d, torch.float32)
+    _need_shape(arrived_bc, "arrived_bc", (replicas.shape[0], _num_packets(d, packet)),
+                torch.uint8)
+    _need_numel(out, "out", 6, torch.float64)
     rp, ld, rt = _rows(replicas, "replicas")
     _check("drift_stats", _load().drift_stats(
         replicas.shape[0], d, packet, rt, rp, ld, _flat(theta, "theta", torch.float32),
@@ -288,11 +410,23 @@ def lossy_step_fused(*, d: int, packet: int, step: int, loss_g: LossSpec, loss_b
                      arrived_b: Optional[torch.Tensor] = None,
                      counts: Optional[torch.Tensor] = None,
                      workspace: Optional[torch.Tensor] = None,
-                     drift: Optional[torch.Tensor] = None, ext: Optional[Ext] = None) -> None:
-    gp, ldg, gt = _rows(grads, "grads")
-    rp, ldr, rt = _rows(replicas, "replicas")
+                     drift: Optional[torch.Tensor] = None, ext=None) -> None:
+    _need_rows(grads, "grads", d)
+    _need_rows(replicas, "replicas", d)
     if replicas.shape[0] != grads.shape[0]:
         raise ValueError("grads and replicas must have the same number of rows")
+    n, P = grads.shape[0], _num_packets(d, packet)
+    for t, name in ((theta, "theta"), (m, "m"), (v, "v")):
+        _need_numel(t, name, d, torch.float32)
+    _need_shape(arrived_g, "arrived_g", (n, P), torch.uint8)
+    _need_shape(arrived_b, "arrived_b", (n, P), torch.uint8)
+    _need_numel(counts, "counts", P, torch.int32)
+    _need_numel(ge_state_g, "ge_state_g", n, torch.uint8)
+    _need_numel(ge_state_b, "ge_state_b", n, torch.uint8)
+    _need_numel(drift, "drift", 6, torch.float64)
+    ref = _ext_ref(ext, n, P, grads)
+    gp, ldg, gt = _rows(grads, "grads")
+    rp, ldr, rt = _rows(replicas, "replicas")
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     _check("lossy_step_fused", _load().lossy_step_fused(
         grads.shape[0], d, packet, step, ctypes.byref(loss_g), ctypes.byref(loss_b),
@@ -301,4 +435,4 @@ def lossy_step_fused(*, d: int, packet: int, step: int, loss_g: LossSpec, loss_b
         _flat(m, "m", torch.float32), _flat(v, "v", torch.float32), rt, rp, ldr,
         _flat(arrived_g, "arrived_g", torch.uint8), _flat(arrived_b, "arrived_b", torch.uint8),
         _flat(counts, "counts", torch.int32), _dev(workspace, "workspace"), ws_bytes,
-        _dev(drift, "drift", torch.float64), _ext_ref(ext), _stream()))
+        _dev(drift, "drift", torch.float64), ref, _stream()))

@@ -16,6 +16,9 @@ using namespace lossy;
 static_assert(sizeof(ll_drift) == sizeof(DriftOut), "ll_drift layout");
 static_assert(sizeof(DriftPartial) == 32, "partial layout");
 static_assert(sizeof(DriftAcc) == 40, "second-level partial layout");
+static_assert(LL_PACE_AUTO == kPaceAuto && LL_PACE_ALWAYS == kPaceAlways &&
+                  LL_PACE_NEVER == kPaceNever,
+              "pacing modes");
 
 namespace {
 
@@ -60,8 +63,7 @@ struct Geometry {
 int check_shape(int32_t n, int64_t d, int64_t packet, Geometry* g) {
     if (n < 1 || n > kMaxWorkers) return fail(LL_EINVAL, "n=%d outside [1, %d]", n, kMaxWorkers);
     if (d < 0) return fail(LL_EINVAL, "d=%lld is negative", (long long)d);
-    if (packet < 8 || packet % 8 != 0)
-        return fail(LL_EINVAL, "packet=%lld must be a positive multiple of 8", (long long)packet);
+    if (packet < 1) return fail(LL_EINVAL, "packet=%lld must be at least 1", (long long)packet);
     g->P = (d + packet - 1) / packet;
     const int64_t chunk = (int64_t)kMinPacketThreads * kElems;
     g->blocks = g->P * ((packet + chunk - 1) / chunk);
@@ -70,10 +72,16 @@ int check_shape(int32_t n, int64_t d, int64_t packet, Geometry* g) {
     return LL_OK;
 }
 
-int check_rows(const char* name, const void* p, int64_t ld, int64_t d) {
+size_t elem_bytes(int32_t dtype) { return dtype == LL_BF16 ? 2 : 4; }
+
+// Rows [n][ld] of elements of `esize` bytes: every row starts on a 16-byte
+// boundary when the base does and ld * esize is a multiple of 16.
+int check_rows(const char* name, const void* p, int64_t ld, int64_t d, size_t esize) {
     if (!p) return fail(LL_EINVAL, "%s is NULL", name);
     if (ld < d) return fail(LL_EINVAL, "%s: ld=%lld < d=%lld", name, (long long)ld, (long long)d);
-    if (ld % 8 != 0) return fail(LL_EALIGN, "%s: ld=%lld not a multiple of 8", name, (long long)ld);
+    if (((size_t)ld * esize) % 16 != 0)
+        return fail(LL_EALIGN, "%s: ld=%lld elements of %zu bytes is not a multiple of 16 bytes",
+                    name, (long long)ld, esize);
     if (!aligned16(p)) return fail(LL_EALIGN, "%s is not 16-byte aligned", name);
     return LL_OK;
 }
@@ -299,9 +307,59 @@ GeJob make_ge_job(const ll_loss* l, int dir, uint8_t* state, uint8_t* arrived,
     return j;
 }
 
+// Long-run fraction of transfers that arrive under a loss process (with
+// parity recovery over groups of g packets when g > 0); only used to lay out
+// the pacing schedule.
+double expected_arrival(const ll_loss* l, int g) {
+    double q;
+    if (l->kind == LL_LOSS_BERNOULLI) {
+        q = 1.0 - l->p;
+    } else {
+        const double s = l->p_gb + l->p_bg;
+        const double bad = s > 0.0 ? l->p_gb / s : 0.0;
+        q = 1.0 - (bad * l->loss_bad + (1.0 - bad) * l->loss_good);
+    }
+    if (g > 0) q = q + (1.0 - q) * std::pow(q, (double)g);
+    return q;
+}
+
 }  // namespace
 
 extern "C" {
+
+int ll_set_pacing(const ll_pacing* cfg) {
+    if (!cfg) return fail(LL_EINVAL, "cfg is NULL");
+    if (cfg->mode != LL_PACE_AUTO && cfg->mode != LL_PACE_ALWAYS && cfg->mode != LL_PACE_NEVER)
+        return fail(LL_EINVAL, "unknown pacing mode %d", cfg->mode);
+    if (!(cfg->bytes_per_s > 0.0 && cfg->bytes_per_s < 1e15))
+        return fail(LL_EINVAL, "bytes_per_s must lie in (0, 1e15)");
+    if (!(cfg->gap_us >= 0.0 && cfg->gap_us <= 1e4))
+        return fail(LL_EINVAL, "gap_us must lie in [0, 1e4]");
+    if (!(cfg->lead_us >= 0.0 && cfg->lead_us <= 1e4))
+        return fail(LL_EINVAL, "lead_us must lie in [0, 1e4]");
+    if (cfg->overlap != 1 && cfg->overlap != 2)
+        return fail(LL_EINVAL, "overlap=%d must be 1 or 2", cfg->overlap);
+    if (cfg->resident < cfg->overlap || cfg->resident > 4)
+        return fail(LL_EINVAL, "resident=%d must lie in [overlap, 4]", cfg->resident);
+    if (!(cfg->headroom > 0.0 && cfg->headroom <= 1.0))
+        return fail(LL_EINVAL, "headroom must lie in (0, 1]");
+    set_pace_setting(PaceSetting{cfg->mode, cfg->bytes_per_s, cfg->gap_us, cfg->lead_us,
+                                 cfg->overlap, cfg->resident, cfg->headroom});
+    return ok();
+}
+
+int ll_get_pacing(ll_pacing* out) {
+    if (!out) return fail(LL_EINVAL, "out is NULL");
+    const PaceSetting st = get_pace_setting();
+    out->mode = st.mode;
+    out->bytes_per_s = st.bytes_per_s;
+    out->gap_us = st.gap_us;
+    out->lead_us = st.lead_us;
+    out->overlap = st.overlap;
+    out->resident = st.resident;
+    out->headroom = st.headroom;
+    return ok();
+}
 
 const char* ll_last_error(void) { return g_error.c_str(); }
 
@@ -368,13 +426,13 @@ int lossy_aggregate(int32_t n, int64_t d, int64_t packet, int32_t gdtype, const 
     if (r) return r;
     if ((r = check_dtype("gdtype", gdtype))) return r;
     if (d == 0) return ok();
-    if ((r = check_rows("grads", grads, ld_g, d))) return r;
+    if ((r = check_rows("grads", grads, ld_g, d, elem_bytes(gdtype)))) return r;
     if (!arrived) return fail(LL_EINVAL, "arrived is NULL");
     if ((r = check_vec("g_hat", g_hat, true))) return r;
     if ((r = check_vec("theta", theta, fallback_lambda != 0.0f))) return r;
     ExtView x;
     if ((r = read_ext(ext, n, &x))) return r;
-    if (x.est == LL_EST_STALE_FILL && (r = check_rows("g_prev", x.g_prev, ld_g, d))) return r;
+    if (x.est == LL_EST_STALE_FILL && (r = check_rows("g_prev", x.g_prev, ld_g, d, elem_bytes(gdtype)))) return r;
     AggParams p;
     if ((r = make_variant(x, x.q, x.g_prev, &p.var))) return r;
     p.n = n;
@@ -429,7 +487,7 @@ int lossy_broadcast(int32_t n, int64_t d, int64_t packet, const float* theta, in
     if ((r = check_dtype("rdtype", rdtype))) return r;
     if (d == 0) return ok();
     if ((r = check_vec("theta", theta, true))) return r;
-    if ((r = check_rows("replicas", replicas, ld_r, d))) return r;
+    if ((r = check_rows("replicas", replicas, ld_r, d, elem_bytes(rdtype)))) return r;
     if (!arrived_bc) return fail(LL_EINVAL, "arrived_bc is NULL");
     BcastParams p;
     p.n = n;
@@ -456,7 +514,7 @@ int drift_stats(int32_t n, int64_t d, int64_t packet, int32_t rdtype, const void
     if ((r = check_vec("out", out, true))) return r;
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     if (d == 0) return hip_check(launch_drift_zero(reinterpret_cast<DriftOut*>(out), s), "drift_stats");
-    if ((r = check_rows("replicas", replicas, ld_r, d))) return r;
+    if ((r = check_rows("replicas", replicas, ld_r, d, elem_bytes(rdtype)))) return r;
     if ((r = check_vec("theta", theta, false))) return r;
     const WsLayout w = ws_layout(n, g);
     if (!workspace || ws_bytes < w.total)
@@ -506,12 +564,12 @@ int lossy_step_fused(int32_t n, int64_t d, int64_t packet, uint64_t step, const 
         if (drift) return hip_check(launch_drift_zero(reinterpret_cast<DriftOut*>(drift), s), "lossy_step_fused");
         return ok();
     }
-    if ((r = check_rows("grads", grads, ld_g, d))) return r;
-    if ((r = check_rows("replicas", replicas, ld_r, d))) return r;
+    if ((r = check_rows("grads", grads, ld_g, d, elem_bytes(gdtype)))) return r;
+    if ((r = check_rows("replicas", replicas, ld_r, d, elem_bytes(rdtype)))) return r;
     if ((r = check_vec("theta", theta, true))) return r;
     OptParams o;
     if ((r = make_opt(opt, step, m, v, &o))) return r;
-    if (x.est == LL_EST_STALE_FILL && (r = check_rows("g_prev", x.g_prev, ld_g, d))) return r;
+    if (x.est == LL_EST_STALE_FILL && (r = check_rows("g_prev", x.g_prev, ld_g, d, elem_bytes(gdtype)))) return r;
     AggVariant var;
     if ((r = fused_variant(x, loss_g, &var))) return r;
     const WsLayout w = ws_layout(n, g);
@@ -546,6 +604,11 @@ int lossy_step_fused(int32_t n, int64_t d, int64_t packet, uint64_t step, const 
     p.groups = drift ? reinterpret_cast<DriftAcc*>(ws + w.groups_off) : nullptr;
     p.var = var;
     p.ages = x.ages;
+    const bool have_ws = workspace && ws_bytes >= w.total && aligned16(workspace);
+    for (int dir = 0; dir < 2; ++dir) {
+        uint8_t* out = dir == 0 ? arrived_g : arrived_b;
+        p.pre[dir] = out ? out : (have_ws ? ws + w.partials + dir * w.masks : nullptr);
+    }
 
     const ll_loss* losses[2] = {loss_g, loss_b};
     uint8_t* states[2] = {ge_state_g, ge_state_b};
@@ -592,7 +655,8 @@ int lossy_step_fused(int32_t n, int64_t d, int64_t packet, uint64_t step, const 
         r = hip_check(launch_masks_ge(L, nge, s), "lossy_step_fused (Gilbert-Elliott masks)");
         if (r) return r;
     }
-    return hip_check(launch_fused(gdtype, rdtype, p, reinterpret_cast<DriftOut*>(drift), s),
+    const PaceHint hint{expected_arrival(loss_g, x.parity), expected_arrival(loss_b, x.parity)};
+    return hip_check(launch_fused(gdtype, rdtype, p, reinterpret_cast<DriftOut*>(drift), hint, s),
                      "lossy_step_fused");
 }
 

@@ -129,6 +129,52 @@ struct FusedParams {
     DriftAcc* groups;  // [kReduceGroups] second-level partials
     AggVariant var;
     uint16_t* ages;    // [n][P] broadcast ages, or null
+    // [n][P] memory where a paced step may draw each direction's Bernoulli
+    // masks beforehand (the caller's mask output or workspace), or null.
+    uint8_t* pre[2];
+};
+
+// Slot schedule of the paced fused step (see ClockPace), times in 1/256
+// clock ticks relative to each round's start.
+struct PaceParams {
+    int64_t per_round;             // workgroups (tiles) per round
+    uint64_t round;                // time between round starts
+    uint64_t off_g, off_r, off_s;  // gradient, replica and stale-read sweep starts
+    uint64_t dg, dr, ds;           // slot lengths of the three sweeps
+    uint64_t guard;                // longest wait, ticks
+};
+
+// Pacing modes and defaults: auto paces steps of at least kPaceMinRounds
+// rounds; the schedule is laid out for kDefaultPaceRate bytes/s with
+// kDefaultPaceGapUs between the gradient and replica sweeps, and starts
+// kPaceMarginUs after the anchor is written.
+enum { kPaceAuto = 0, kPaceAlways = 1, kPaceNever = 2 };
+constexpr int64_t kPaceMinRounds = 8;
+constexpr double kDefaultPaceRate = 6.0e12;
+constexpr double kDefaultPaceGapUs = 2.0;
+constexpr double kDefaultPaceLeadUs = 2.5;
+constexpr int kDefaultPaceOverlap = 2;
+constexpr int kDefaultPaceResident = 2;
+constexpr double kPaceMarginUs = 5.0;
+// Fraction of the resident workgroup places the rounds in flight may fill.
+constexpr double kDefaultPaceHeadroom = 0.9;
+
+// How the fused step is paced (process-wide; see ll_set_pacing).
+struct PaceSetting {
+    int mode;            // 0 auto, 1 always, 2 never
+    double bytes_per_s;  // rate the schedule is laid out for
+    double gap_us;       // allowance between the last gradient row and the first replica row
+    double lead_us;      // allowance from a round's start to its first gradient row
+    int overlap;         // rounds streaming at once (1 or 2)
+    int resident;        // rounds the resident workgroup places are shared by (>= overlap)
+    double headroom;     // fraction of the resident places the rounds may fill
+};
+PaceSetting get_pace_setting();
+void set_pace_setting(const PaceSetting& s);
+
+// Expected arrival probabilities of a step, for laying out its schedule.
+struct PaceHint {
+    double q_g, q_b;
 };
 
 // Largest packet group of the parity-packet recovery.
@@ -165,7 +211,7 @@ hipError_t launch_broadcast(int rdtype, const BcastParams& p, hipStream_t s);
 hipError_t launch_drift(int rdtype, const DriftParams& p, int n, int64_t d, int have_master,
                         DriftOut* out, hipStream_t s);
 hipError_t launch_fused(int gdtype, int rdtype, const FusedParams& p, DriftOut* drift,
-                        hipStream_t s);
+                        const PaceHint& hint, hipStream_t s);
 hipError_t launch_drift_zero(DriftOut* out, hipStream_t s);
 
 }  // namespace lossy

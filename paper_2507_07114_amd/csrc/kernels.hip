@@ -14,6 +14,11 @@
 
 #include <math.h>
 
+#include <atomic>
+#include <map>
+#include <mutex>
+#include <utility>
+
 namespace lossy {
 
 // ---------------------------------------------------------------------------
@@ -204,25 +209,49 @@ struct Chunk {
     int c;        // chunk within the packet
     int64_t e0;   // first element of this thread
     int nv;       // valid elements of this thread (0..8)
+    bool whole;   // wave-uniform: every thread owns 0 or 8 elements, 16-byte aligned
 };
 
+// Chunk of tile b (tile = packet * cpp + chunk within the packet).  A chunk
+// is whole when it starts on a multiple of 8 elements and its valid part
+// ends on one or fills it: then every access of the tile can be a 16-byte
+// vector (row starts are 16-byte aligned).
 template <int NT>
-__device__ __forceinline__ Chunk chunk_of(int64_t d, int64_t L, int cpp) {
+__device__ __forceinline__ Chunk chunk_at(int64_t b, int64_t d, int64_t L, int cpp) {
     Chunk ch;
-    const int64_t b = blockIdx.x;
     ch.k = b / cpp;
     ch.c = (int)(b - ch.k * cpp);
     const int64_t pk0 = ch.k * L;
     const int64_t pend = pk0 + L < d ? pk0 + L : d;
-    ch.e0 = pk0 + (int64_t)ch.c * (NT * kElems) + (int64_t)threadIdx.x * kElems;
+    const int64_t c0 = pk0 + (int64_t)ch.c * (NT * kElems);
+    ch.e0 = c0 + (int64_t)threadIdx.x * kElems;
     const int64_t rem = pend - ch.e0;
     ch.nv = rem <= 0 ? 0 : (rem >= 8 ? 8 : (int)rem);
+    ch.whole = (c0 % 8 == 0) && ((pend - c0) % 8 == 0 || pend >= c0 + NT * kElems);
     return ch;
+}
+
+template <int NT>
+__device__ __forceinline__ Chunk chunk_of(int64_t d, int64_t L, int cpp) {
+    return chunk_at<NT>(blockIdx.x, d, L, cpp);
 }
 
 // ---------------------------------------------------------------------------
 // One-stage entry points
 // ---------------------------------------------------------------------------
+template <class G, bool W>
+__device__ __forceinline__ void aggregate_chunk(const AggParams& p, const Chunk& ch,
+                                                const uint64_t* words, int nw, int K) {
+    float th[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+    if (K == 0 && p.lam != 0.0f && p.var.kind == kEstArrivedMean)
+        load8<F32, W>(p.theta + ch.e0, ch.nv, th);
+    const bool relp = p.var.reliable != nullptr && p.var.reliable[ch.k] != 0;
+    float g[8];
+    aggregate8<G, W>(reinterpret_cast<const typename G::T*>(p.grads), p.ld, ch.e0, ch.nv, words,
+                     nw, p.n, K, p.lam, th, p.var, relp, NoPace(), g);
+    store_f32x8<W>(p.g_hat + ch.e0, ch.nv, g);
+}
+
 template <class G>
 __global__ __launch_bounds__(G::kPacketThreads) void k_aggregate(AggParams p) {
     constexpr int NT = G::kPacketThreads;
@@ -235,31 +264,51 @@ __global__ __launch_bounds__(G::kPacketThreads) void k_aggregate(AggParams p) {
     const int K = popcount_words(s_words[0], nw);
     if (ch.c == 0 && threadIdx.x == 0 && p.counts) p.counts[ch.k] = K;
     if (ch.nv == 0) return;
-    float th[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-    if (K == 0 && p.lam != 0.0f && p.var.kind == kEstArrivedMean)
-        load_f32x8(p.theta + ch.e0, ch.nv, th);
-    const bool relp = p.var.reliable != nullptr && p.var.reliable[ch.k] != 0;
-    float g[8];
-    aggregate8<G>(reinterpret_cast<const typename G::T*>(p.grads), p.ld, ch.e0, ch.nv,
-                  s_words[0], nw, p.n, K, p.lam, th, p.var, relp, g);
-    store_f32x8(p.g_hat + ch.e0, ch.nv, g);
+    if (ch.whole) aggregate_chunk<G, true>(p, ch, s_words[0], nw, K);
+    else aggregate_chunk<G, false>(p, ch, s_words[0], nw, K);
+}
+
+template <bool W>
+__device__ __forceinline__ void shard_step8(int64_t e0, int nv, const OptParams& o, float* theta,
+                                            float* m, float* v, const float* g_hat) {
+    float th[8], mm[8], vv[8], g[8];
+    load8<F32, W>(theta + e0, nv, th);
+    load8<F32, W>(g_hat + e0, nv, g);
+    if (o.kind >= 1) load8<F32, W>(m + e0, nv, mm);
+    if (o.kind == 2) load8<F32, W>(v + e0, nv, vv);
+    update8(o, th, mm, vv, g);
+    store_f32x8<W>(theta + e0, nv, th);
+    if (o.kind >= 1) store_f32x8<W>(m + e0, nv, mm);
+    if (o.kind == 2) store_f32x8<W>(v + e0, nv, vv);
 }
 
 __global__ __launch_bounds__(kThreads) void k_shard_step(int64_t d, OptParams o, float* theta,
                                                          float* m, float* v,
                                                          const float* g_hat) {
-    const int64_t e0 = ((int64_t)blockIdx.x * kThreads + threadIdx.x) * kElems;
+    const int64_t b0 = (int64_t)blockIdx.x * kThreads * kElems;
+    const int64_t e0 = b0 + (int64_t)threadIdx.x * kElems;
     if (e0 >= d) return;
     const int nv = d - e0 >= 8 ? 8 : (int)(d - e0);
-    float th[8], mm[8], vv[8], g[8];
-    load_f32x8(theta + e0, nv, th);
-    load_f32x8(g_hat + e0, nv, g);
-    if (o.kind >= 1) load_f32x8(m + e0, nv, mm);
-    if (o.kind == 2) load_f32x8(v + e0, nv, vv);
-    update8(o, th, mm, vv, g);
-    store_f32x8(theta + e0, nv, th);
-    if (o.kind >= 1) store_f32x8(m + e0, nv, mm);
-    if (o.kind == 2) store_f32x8(v + e0, nv, vv);
+    if (d % 8 == 0 || d >= b0 + kThreads * kElems) shard_step8<true>(e0, nv, o, theta, m, v, g_hat);
+    else shard_step8<false>(e0, nv, o, theta, m, v, g_hat);
+}
+
+template <class R, bool W>
+__device__ __forceinline__ void broadcast_chunk(const BcastParams& p, const Chunk& ch,
+                                                const uint64_t* words, int nw) {
+    float th[8];
+    load8<F32, W>(p.theta + ch.e0, ch.nv, th);
+    Packed8<R> r;
+    r.pack(th);
+    typename R::T* reps = reinterpret_cast<typename R::T*>(p.replicas);
+    for (int w = 0; w < nw; ++w) {
+        uint64_t bits = uniform64(words[w]);
+        while (bits) {
+            const int i = w * 64 + __builtin_ctzll(bits);
+            bits &= bits - 1;
+            r.template store<W>(reps + (int64_t)i * p.ld + ch.e0, ch.nv);
+        }
+    }
 }
 
 template <class R>
@@ -272,22 +321,48 @@ __global__ __launch_bounds__(R::kPacketThreads) void k_broadcast(BcastParams p) 
     stage_masks<NT>(1, &src, p.n, p.P, ch.k, 0, dirs, s_words);
     if (ch.nv == 0) return;
     const int nw = (p.n + 63) >> 6;
-    float th[8];
-    load_f32x8(p.theta + ch.e0, ch.nv, th);
-    Packed8<R> r;
-    r.pack(th);
-    typename R::T* reps = reinterpret_cast<typename R::T*>(p.replicas);
-    for (int w = 0; w < nw; ++w) {
-        uint64_t bits = uniform64(s_words[0][w]);
-        while (bits) {
-            const int i = w * 64 + __builtin_ctzll(bits);
-            bits &= bits - 1;
-            r.store(reps + (int64_t)i * p.ld + ch.e0, ch.nv);
-        }
-    }
+    if (ch.whole) broadcast_chunk<R, true>(p, ch, s_words[0], nw);
+    else broadcast_chunk<R, false>(p, ch, s_words[0], nw);
 }
 
-// Drift over all rows of the chunk (rows read in ascending order).
+// Drift of one chunk over all rows, read in ascending order.
+template <class R, bool W>
+__device__ __forceinline__ void drift_chunk(const DriftParams& p, const Chunk& ch, double& pair,
+                                            double& range, double& abs_sum) {
+    const typename R::T* reps = reinterpret_cast<const typename R::T*>(p.replicas);
+    float r[8];
+    if (p.theta) {
+        float th[8];
+        load8<F32, W>(p.theta + ch.e0, ch.nv, th);
+        Packed8<R> pr;
+        pr.pack(th);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) r[j] = pr.value(j);
+    } else {
+        load8<R, W>(reps + ch.e0, ch.nv, r);
+    }
+    Drift8 acc;
+    acc.init(false, r);
+    for (int i0 = 0; i0 < p.n; i0 += kBatchDrift) {
+        Raw8<R> raw[kBatchDrift];
+#pragma unroll
+        for (int u = 0; u < kBatchDrift; ++u) {
+            const int row = i0 + u < p.n ? i0 + u : i0;
+            load_raw<W>(reps + (int64_t)row * p.ld + ch.e0, ch.nv, raw[u]);
+        }
+#pragma unroll
+        for (int u = 0; u < kBatchDrift; ++u) {
+            if (i0 + u < p.n) {
+                float x[8];
+                unpack(raw[u], x);
+                acc.add(x, r, ch.nv);
+            }
+        }
+    }
+    acc.finish(p.n, ch.nv, pair, range);
+    abs_sum = acc.abs_sum;
+}
+
 template <class R>
 __global__ __launch_bounds__(R::kPacketThreads) void k_drift(DriftParams p) {
     constexpr int NT = R::kPacketThreads;
@@ -301,35 +376,10 @@ __global__ __launch_bounds__(R::kPacketThreads) void k_drift(DriftParams p) {
         stage_masks<NT>(1, &src, p.n, p.P, ch.k, 0, dirs, s_words);
         if (ch.c == 0) stale = (uint32_t)(p.n - popcount_words(s_words[0], nw));
     }
-    const typename R::T* reps = reinterpret_cast<const typename R::T*>(p.replicas);
     double pair = 0.0, range = 0.0, abs_sum = 0.0;
     if (ch.nv > 0) {
-        float r[8];
-        if (p.theta) {
-            float th[8];
-            load_f32x8(p.theta + ch.e0, ch.nv, th);
-            Packed8<R> pr;
-            pr.pack(th);
-#pragma unroll
-            for (int j = 0; j < 8; ++j) r[j] = pr.value(j);
-        } else {
-            load8<R>(reps + ch.e0, ch.nv, r);
-        }
-        Drift8 acc;
-        acc.init(false, r);
-        for (int i0 = 0; i0 < p.n; i0 += kBatchDrift) {
-            float x[kBatchDrift][8];
-#pragma unroll
-            for (int u = 0; u < kBatchDrift; ++u) {
-                const int row = i0 + u < p.n ? i0 + u : i0;
-                load8<R>(reps + (int64_t)row * p.ld + ch.e0, ch.nv, x[u]);
-            }
-#pragma unroll
-            for (int u = 0; u < kBatchDrift; ++u)
-                if (i0 + u < p.n) acc.add(x[u], r, ch.nv);
-        }
-        acc.finish(p.n, ch.nv, pair, range);
-        abs_sum = acc.abs_sum;
+        if (ch.whole) drift_chunk<R, true>(p, ch, pair, range, abs_sum);
+        else drift_chunk<R, false>(p, ch, pair, range, abs_sum);
     }
     block_reduce_partial<NT>(pair, abs_sum, range, stale, 0, p.partials + blockIdx.x);
 }
@@ -431,11 +481,94 @@ static hipError_t launch_drift_reduce(const DriftPartial* parts, int64_t count, 
 // theta/m/v (read and written once), the arrived replica rows (written
 // once) and, with drift, the stale replica rows (read once).
 // ---------------------------------------------------------------------------
-template <class G, class R, bool DRIFT>
-__global__ __launch_bounds__(R::kPacketThreads) void k_step_fused(FusedParams p) {
+// The per-element part of one tile of the fused step (threads with nv > 0):
+// aggregate, update, broadcast and, with DRIFT, the stale rows' drift sums.
+template <class G, class R, bool DRIFT, bool W, class Pace>
+__device__ __forceinline__ void step_chunk(const FusedParams& p, const Chunk& ch, const Pace& pace,
+                                           const uint64_t (*s_words)[kMaxWords], int nw, int K,
+                                           int RC, const Raw8<F32>& th_r, const Raw8<F32>& m_r,
+                                           const Raw8<F32>& v_r, double& pair, double& range,
+                                           double& abs_sum) {
+    const bool relp = p.var.reliable != nullptr && p.var.reliable[ch.k] != 0;
+    AggVariant var = p.var;
+    if (var.parity_group > 0 && !relp) var.invq = parity_invq(var, ch.k, p.P);
+    if (var.ge_derived && !relp) var.invq = ge_invq(var, p.step, ch.k, p.P);
+    float th[8], mm[8], vv[8], g[8];
+    unpack(th_r, th);
+    aggregate8<G, W>(reinterpret_cast<const typename G::T*>(p.grads), p.ld_g, ch.e0, ch.nv,
+                     s_words[0], nw, p.n, K, p.lam, th, var, relp, pace, g);
+    if (p.opt.kind >= 1) unpack(m_r, mm);
+    if (p.opt.kind == 2) unpack(v_r, vv);
+    update8(p.opt, th, mm, vv, g);
+    store_f32x8<W>(p.theta + ch.e0, ch.nv, th);
+    if (p.opt.kind >= 1) store_f32x8<W>(p.m + ch.e0, ch.nv, mm);
+    if (p.opt.kind == 2) store_f32x8<W>(p.v + ch.e0, ch.nv, vv);
+
+    Packed8<R> r;
+    r.pack(th);
+    typename R::T* reps = reinterpret_cast<typename R::T*>(p.replicas);
+    const int last_bits = p.n - (nw - 1) * 64;
+    for (int w = 0; w < nw; ++w) {
+        const uint64_t valid = (w == nw - 1 && last_bits < 64) ? ((1ull << last_bits) - 1) : ~0ull;
+        uint64_t bits = uniform64(s_words[1][w]) & valid;
+        while (bits) {
+            const int i = w * 64 + __builtin_ctzll(bits);
+            bits &= bits - 1;
+            pace.rep(i);
+            r.template store<W>(reps + (int64_t)i * p.ld_r + ch.e0, ch.nv);
+        }
+    }
+    if (!DRIFT) return;
+    // Stale rows (broadcast lost) in ascending order, after every store.
+    Drift8 acc;
+    float rv[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) rv[j] = r.value(j);
+    acc.init(RC > 0, rv);
+    for (int w = 0; w < nw; ++w) {
+        const uint64_t valid = (w == nw - 1 && last_bits < 64) ? ((1ull << last_bits) - 1) : ~0ull;
+        uint64_t sb = ~uniform64(s_words[1][w]) & valid;
+        while (sb) {
+            int idx[kBatchStale];
+#pragma unroll
+            for (int u = 0; u < kBatchStale; ++u) {
+                idx[u] = sb ? (w * 64 + __builtin_ctzll(sb)) : -1;
+                sb &= sb - 1;
+            }
+            Raw8<R> raw[kBatchStale];
+#pragma unroll
+            for (int u = 0; u < kBatchStale; ++u) {
+                const int row = idx[u] >= 0 ? idx[u] : idx[0];
+                pace.stale(row);
+                load_raw<W>(reps + (int64_t)row * p.ld_r + ch.e0, ch.nv, raw[u]);
+            }
+#pragma unroll
+            for (int u = 0; u < kBatchStale; ++u) {
+                if (idx[u] >= 0) {
+                    float x[8];
+                    unpack(raw[u], x);
+                    acc.add(x, rv, ch.nv);
+                }
+            }
+        }
+    }
+    acc.finish(p.n, ch.nv, pair, range);
+    abs_sum = acc.abs_sum;
+}
+
+// One tile (a chunk of one packet) of the fused step in access form W.  The
+// master and moments are requested before the masks are staged, so their
+// latency overlaps the mask draws.
+template <class G, class R, bool DRIFT, bool W, class Pace>
+__device__ __forceinline__ void step_tile_w(const FusedParams& p, const Chunk& ch, int64_t tile,
+                                            const Pace& pace, uint64_t (*s_words)[kMaxWords]) {
     constexpr int NT = R::kPacketThreads;
-    __shared__ uint64_t s_words[2][kMaxWords];
-    const Chunk ch = chunk_of<NT>(p.d, p.L, p.cpp);
+    Raw8<F32> th_r, m_r, v_r;
+    if (ch.nv > 0) {
+        load_raw<W>(p.theta + ch.e0, ch.nv, th_r);
+        if (p.opt.kind >= 1) load_raw<W>(p.m + ch.e0, ch.nv, m_r);
+        if (p.opt.kind == 2) load_raw<W>(p.v + ch.e0, ch.nv, v_r);
+    }
     const int dirs[2] = {0, 1};
     stage_masks<NT>(2, p.src, p.n, p.P, ch.k, p.step, dirs, s_words);
     const int nw = (p.n + 63) >> 6;
@@ -454,73 +587,71 @@ __global__ __launch_bounds__(R::kPacketThreads) void k_step_fused(FusedParams p)
     }
 
     double pair = 0.0, range = 0.0, abs_sum = 0.0;
-    if (ch.nv > 0) {
-        float th[8], mm[8], vv[8], g[8];
-        load_f32x8(p.theta + ch.e0, ch.nv, th);
-        if (p.opt.kind >= 1) load_f32x8(p.m + ch.e0, ch.nv, mm);
-        if (p.opt.kind == 2) load_f32x8(p.v + ch.e0, ch.nv, vv);
-        const bool relp = p.var.reliable != nullptr && p.var.reliable[ch.k] != 0;
-        AggVariant var = p.var;
-        if (var.parity_group > 0 && !relp) var.invq = parity_invq(var, ch.k, p.P);
-        if (var.ge_derived && !relp) var.invq = ge_invq(var, p.step, ch.k, p.P);
-        aggregate8<G>(reinterpret_cast<const typename G::T*>(p.grads), p.ld_g, ch.e0, ch.nv,
-                      s_words[0], nw, p.n, K, p.lam, th, var, relp, g);
-        update8(p.opt, th, mm, vv, g);
-        store_f32x8(p.theta + ch.e0, ch.nv, th);
-        if (p.opt.kind >= 1) store_f32x8(p.m + ch.e0, ch.nv, mm);
-        if (p.opt.kind == 2) store_f32x8(p.v + ch.e0, ch.nv, vv);
-
-        Packed8<R> r;
-        r.pack(th);
-        typename R::T* reps = reinterpret_cast<typename R::T*>(p.replicas);
-        Drift8 acc;
-        float rv[8];
-        if (DRIFT) {
-#pragma unroll
-            for (int j = 0; j < 8; ++j) rv[j] = r.value(j);
-            acc.init(RC > 0, rv);
-        }
-        const int last_bits = p.n - (nw - 1) * 64;
-        for (int w = 0; w < nw; ++w) {
-            const uint64_t valid = (w == nw - 1 && last_bits < 64) ? ((1ull << last_bits) - 1) : ~0ull;
-            const uint64_t bm = uniform64(s_words[1][w]);
-            uint64_t bits = bm & valid;
-            while (bits) {
-                const int i = w * 64 + __builtin_ctzll(bits);
-                bits &= bits - 1;
-                r.store(reps + (int64_t)i * p.ld_r + ch.e0, ch.nv);
-            }
-            if (DRIFT) {
-                uint64_t sb = ~bm & valid;
-                while (sb) {
-                    int idx[kBatchStale];
-#pragma unroll
-                    for (int u = 0; u < kBatchStale; ++u) {
-                        idx[u] = sb ? (w * 64 + __builtin_ctzll(sb)) : -1;
-                        sb &= sb - 1;
-                    }
-                    float x[kBatchStale][8];
-#pragma unroll
-                    for (int u = 0; u < kBatchStale; ++u) {
-                        const int row = idx[u] >= 0 ? idx[u] : idx[0];
-                        load8<R>(reps + (int64_t)row * p.ld_r + ch.e0, ch.nv, x[u]);
-                    }
-#pragma unroll
-                    for (int u = 0; u < kBatchStale; ++u)
-                        if (idx[u] >= 0) acc.add(x[u], rv, ch.nv);
-                }
-            }
-        }
-        if (DRIFT) {
-            acc.finish(p.n, ch.nv, pair, range);
-            abs_sum = acc.abs_sum;
-        }
-    }
+    if (ch.nv > 0)
+        step_chunk<G, R, DRIFT, W>(p, ch, pace, s_words, nw, K, RC, th_r, m_r, v_r, pair, range,
+                                   abs_sum);
     if (DRIFT) {
         const uint32_t stale = ch.c == 0 ? (uint32_t)(p.n - RC) : 0u;
         const uint32_t empty = (ch.c == 0 && K == 0) ? 1u : 0u;
-        block_reduce_partial<NT>(pair, abs_sum, range, stale, empty, p.partials + blockIdx.x);
+        block_reduce_partial<NT>(pair, abs_sum, range, stale, empty, p.partials + tile);
     }
+}
+
+// One tile (a chunk of one packet) of the fused step.  All NT threads of the
+// workgroup call it; it stages the tile's masks in s_words (ending with a
+// barrier).  `pace` delays row accesses (NoPace: none); it never changes
+// what is computed.
+template <class G, class R, bool DRIFT, class Pace>
+__device__ __forceinline__ void step_tile(const FusedParams& p, int64_t tile, const Pace& pace,
+                                          uint64_t (*s_words)[kMaxWords]) {
+    constexpr int NT = R::kPacketThreads;
+    const Chunk ch = chunk_at<NT>(tile, p.d, p.L, p.cpp);
+    if (ch.whole) step_tile_w<G, R, DRIFT, true>(p, ch, tile, pace, s_words);
+    else step_tile_w<G, R, DRIFT, false>(p, ch, tile, pace, s_words);
+}
+
+// One tile per workgroup.
+template <class G, class R, bool DRIFT>
+__global__ __launch_bounds__(R::kPacketThreads) void k_step_fused(FusedParams p) {
+    __shared__ uint64_t s_words[2][kMaxWords];
+    step_tile<G, R, DRIFT>(p, blockIdx.x, NoPace(), s_words);
+}
+
+// Anchor of the paced step's schedule: the clock time its first round
+// starts, written by a one-lane kernel launched just before the step.  One
+// anchor per device; overlapping paced steps on one device may read each
+// other's anchor, which can cost speed but never changes a result.
+__device__ uint64_t g_pace_anchor;
+
+__global__ void k_pace_anchor(uint64_t margin_ticks) {
+    if (threadIdx.x == 0)
+        __hip_atomic_store(&g_pace_anchor, clock_ticks() + margin_ticks, __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Paced step: one tile per workgroup as in k_step_fused, tile b in round
+// b / per_round, per_round no more than the workgroups the chip holds at
+// once.  Round r's row accesses follow the slot schedule anchored at
+// g_pace_anchor + r * round; the workgroups of round r + 1 take the places
+// of round r's as those finish, around the time their own round starts.  A
+// round covers adjacent tiles, so at any slot the chip streams a few long
+// runs of one row instead of scattered pieces of every row.
+template <class G, class R, bool DRIFT>
+__global__ __launch_bounds__(R::kPacketThreads) void k_step_paced(FusedParams p, PaceParams q) {
+    __shared__ uint64_t s_words[2][kMaxWords];
+    const uint64_t t0 =
+        __hip_atomic_load(&g_pace_anchor, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    const uint64_t r = (uint64_t)blockIdx.x / (uint64_t)q.per_round;
+    ClockPace pace;
+    pace.base = t0 + ((r * q.round) >> 8);
+    pace.off_g = q.off_g;
+    pace.off_r = q.off_r;
+    pace.off_s = q.off_s;
+    pace.dg = q.dg;
+    pace.dr = q.dr;
+    pace.ds = q.ds;
+    pace.guard = q.guard;
+    step_tile<G, R, DRIFT>(p, blockIdx.x, pace, s_words);
 }
 
 __global__ void k_drift_zero(DriftOut* out) {
@@ -640,27 +771,187 @@ hipError_t launch_drift(int rdtype, const DriftParams& p, int n, int64_t d, int 
     return launch_drift_reduce(p.partials, blocks, p.groups, n, d, have_master, out, s);
 }
 
+// ---------------------------------------------------------------------------
+// Pacing of the fused step
+// ---------------------------------------------------------------------------
+namespace {
+std::atomic<int> g_pace_mode{0};
+std::atomic<double> g_pace_rate{kDefaultPaceRate};
+std::atomic<double> g_pace_gap_us{kDefaultPaceGapUs};
+std::atomic<double> g_pace_lead_us{kDefaultPaceLeadUs};
+std::atomic<int> g_pace_overlap{kDefaultPaceOverlap};
+std::atomic<int> g_pace_resident{kDefaultPaceResident};
+std::atomic<double> g_pace_headroom{kDefaultPaceHeadroom};
+
+// Compute units and clock rate of a device, and resident workgroups per
+// compute unit of a kernel, looked up once.
+std::mutex g_cache_mu;
+std::map<int, std::pair<int, double>> g_dev_cache;
+std::map<std::pair<int, const void*>, int> g_occ_cache;
+
+bool device_info(int dev, int* cus, double* tick_hz) {
+    std::lock_guard<std::mutex> lk(g_cache_mu);
+    auto it = g_dev_cache.find(dev);
+    if (it == g_dev_cache.end()) {
+        int c = 0, khz = 0;
+        if (hipDeviceGetAttribute(&c, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+            hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, dev) != hipSuccess)
+            return false;
+        it = g_dev_cache.emplace(dev, std::make_pair(c, 1e3 * (double)khz)).first;
+    }
+    *cus = it->second.first;
+    *tick_hz = it->second.second;
+    return *cus > 0 && *tick_hz > 0.0;
+}
+
+template <class K>
+int resident_per_cu(int dev, K kernel, int threads) {
+    const void* key = reinterpret_cast<const void*>(kernel);
+    {
+        std::lock_guard<std::mutex> lk(g_cache_mu);
+        auto it = g_occ_cache.find({dev, key});
+        if (it != g_occ_cache.end()) return it->second;
+    }
+    int nb = 0;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, kernel, threads, 0) != hipSuccess) nb = 0;
+    std::lock_guard<std::mutex> lk(g_cache_mu);
+    g_occ_cache[{dev, key}] = nb;
+    return nb;
+}
+}  // namespace
+
+PaceSetting get_pace_setting() {
+    return PaceSetting{g_pace_mode.load(), g_pace_rate.load(), g_pace_gap_us.load(),
+                       g_pace_lead_us.load(), g_pace_overlap.load(), g_pace_resident.load(),
+                       g_pace_headroom.load()};
+}
+
+void set_pace_setting(const PaceSetting& st) {
+    g_pace_mode.store(st.mode);
+    g_pace_rate.store(st.bytes_per_s);
+    g_pace_gap_us.store(st.gap_us);
+    g_pace_lead_us.store(st.lead_us);
+    g_pace_overlap.store(st.overlap);
+    g_pace_resident.store(st.resident);
+    g_pace_headroom.store(st.headroom);
+}
+
+// Lay out the schedule of a paced step with `tiles` tiles, or return false
+// to run it unpaced.  `overlap` rounds stream at once, each covering *grid
+// adjacent tiles (`resident` rounds fill at most kPaceHeadroom of the
+// resident workgroup places; rounds are balanced) and laid out for its
+// share, rate / overlap, of the bandwidth.  A round is: a
+// lead for the workgroups to start, draw masks and read their master and
+// moments; the gradient sweep; the gap for the update and the master and
+// moment writes; the replica sweep; the stale-read sweep.  Each sweep's slot
+// lasts as long as the rows that slot is expected to move take at the
+// round's share.  Rounds start round / overlap apart, so with two in flight
+// one round's gradient sweep runs beside the previous round's replica sweep
+// and each round's lead, gap and tail are covered by the other's streams.
+template <class G, class R, bool DRIFT>
+static bool pace_plan(const FusedParams& p, const PaceHint& h, int64_t tiles, PaceParams* q,
+                      int64_t* grid, uint64_t* margin) {
+    constexpr int NT = R::kPacketThreads;
+    const PaceSetting st = get_pace_setting();
+    if (st.mode == kPaceNever || !(st.bytes_per_s > 0.0) || tiles <= 0) return false;
+    int dev = 0, cus = 0;
+    double tick_hz = 0.0;
+    if (hipGetDevice(&dev) != hipSuccess || !device_info(dev, &cus, &tick_hz)) return false;
+    const int per_cu = resident_per_cu(dev, k_step_paced<G, R, DRIFT>, NT);
+    const int k = st.overlap < 1 ? 1 : (st.overlap > 2 ? 2 : st.overlap);
+    const int res = st.resident < k ? k : st.resident;
+    const int64_t gmax = (int64_t)(st.headroom * per_cu * cus / res);
+    if (gmax < 1) return false;
+    const int64_t rounds = (tiles + gmax - 1) / gmax;
+    if (st.mode == kPaceAuto && rounds < kPaceMinRounds) return false;
+    const int64_t g = (tiles + rounds - 1) / rounds;
+    const double row_g = (double)NT * kElems * sizeof(typename G::T);
+    const double row_r = (double)NT * kElems * sizeof(typename R::T);
+    const double state = (double)NT * kElems * 4.0 * (p.opt.kind + 1);
+    const double fp = 256.0 * tick_hz * k / st.bytes_per_s;  // 1/256 ticks per byte of a round
+    const double us = 1e-6 * tick_hz * 256.0;                 // 1/256 ticks per microsecond
+    const double qg = h.q_g < 0.0 ? 0.0 : (h.q_g > 1.0 ? 1.0 : h.q_g);
+    const double qb = h.q_b < 0.0 ? 0.0 : (h.q_b > 1.0 ? 1.0 : h.q_b);
+    const double n = (double)p.n;
+    const double dg = g * row_g * qg * fp;
+    const double dr = g * row_r * qb * fp;
+    const double ds = DRIFT ? g * row_r * (1.0 - qb) * fp : 0.0;
+    const double off_g = st.lead_us * us + g * state * fp;
+    const double off_r = off_g + n * dg + g * state * fp + st.gap_us * us;
+    const double off_s = off_r + n * dr;
+    const double length = off_s + n * ds;
+    // Rounds start `spacing` apart: no closer than the round's bytes at its
+    // share allow with k rounds streaming (stream / k), and far enough apart
+    // that a round's workgroups find places when it starts, res rounds
+    // sharing the resident places (length / res).  With k = 2 and res = 3
+    // the lead, gap and tail of each round are covered by the other rounds'
+    // streams.
+    const double stream = n * (dg + dr + ds) + 2.0 * g * state * fp;
+    const double spacing = stream / k > length / res ? stream / k : length / res;
+    if (!(length < 1e15)) return false;
+    q->per_round = g;
+    q->dg = (uint64_t)dg;
+    q->dr = (uint64_t)dr;
+    q->ds = (uint64_t)ds;
+    q->off_g = (uint64_t)off_g;
+    q->off_r = (uint64_t)off_r;
+    q->off_s = (uint64_t)off_s;
+    q->round = (uint64_t)spacing;
+    *margin = (uint64_t)(kPaceMarginUs * 1e-6 * tick_hz) + 1;
+    q->guard = 2 * ((uint64_t)length >> 8) + 2 * *margin + 1;
+    *grid = g;
+    return true;
+}
+
 // The fused step's geometry follows the replica type, like the standalone
 // drift kernel, so both fold drift partials over the same partition.
-template <class G, class R>
-static int64_t launch_fused_gr(bool drift, FusedParams p, hipStream_t s) {
+template <class G, class R, bool DRIFT>
+static int64_t launch_fused_grd(const FusedParams& p, const PaceHint& h, hipStream_t s) {
     constexpr int NT = R::kPacketThreads;
-    const int64_t blocks = packet_grid<NT>(p.P, p.L, &p.cpp);
-    if (drift)
-        hipLaunchKernelGGL((k_step_fused<G, R, true>), dim3((unsigned)blocks), dim3(NT), 0, s, p);
-    else
-        hipLaunchKernelGGL((k_step_fused<G, R, false>), dim3((unsigned)blocks), dim3(NT), 0, s, p);
-    return blocks;
+    FusedParams pp = p;
+    const int64_t tiles = packet_grid<NT>(pp.P, pp.L, &pp.cpp);
+    PaceParams q;
+    int64_t grid = 0;
+    uint64_t margin = 0;
+    if (pace_plan<G, R, DRIFT>(pp, h, tiles, &q, &grid, &margin)) {
+        // Bernoulli masks drawn in the step would put every workgroup's
+        // draws at the start of its round, all at once; where memory for
+        // them is at hand they are drawn beforehand by the mask kernel and
+        // the step reads them.
+        for (int dir = 0; dir < 2; ++dir) {
+            if (!pp.src[dir].draw || !pp.pre[dir]) continue;
+            const MaskSource& m = pp.src[dir];
+            hipError_t e = launch_masks_bernoulli(pp.n, pp.P, pp.step, dir, m.seed, m.thr, m.owner,
+                                                  m.reliable, pp.pre[dir], s);
+            if (e != hipSuccess) return -1;
+            pp.src[dir] = MaskSource{false, 0, 0, pp.pre[dir], -1, nullptr};
+            if (dir == 0 && pp.out_g == pp.pre[0]) pp.out_g = nullptr;
+            if (dir == 1 && pp.out_b == pp.pre[1]) pp.out_b = nullptr;
+        }
+        hipLaunchKernelGGL(k_pace_anchor, dim3(1), dim3(64), 0, s, margin);
+        hipLaunchKernelGGL((k_step_paced<G, R, DRIFT>), dim3((unsigned)tiles), dim3(NT), 0, s, pp,
+                           q);
+    } else {
+        hipLaunchKernelGGL((k_step_fused<G, R, DRIFT>), dim3((unsigned)tiles), dim3(NT), 0, s, pp);
+    }
+    return tiles;
+}
+
+template <class G, class R>
+static int64_t launch_fused_gr(bool drift, const FusedParams& p, const PaceHint& h,
+                               hipStream_t s) {
+    return drift ? launch_fused_grd<G, R, true>(p, h, s) : launch_fused_grd<G, R, false>(p, h, s);
 }
 
 hipError_t launch_fused(int gdtype, int rdtype, const FusedParams& p, DriftOut* drift,
-                        hipStream_t s) {
+                        const PaceHint& h, hipStream_t s) {
     const bool dr = drift != nullptr;
     int64_t blocks;
-    if (gdtype == 1 && rdtype == 1) blocks = launch_fused_gr<BF16, BF16>(dr, p, s);
-    else if (gdtype == 1) blocks = launch_fused_gr<BF16, F32>(dr, p, s);
-    else if (rdtype == 1) blocks = launch_fused_gr<F32, BF16>(dr, p, s);
-    else blocks = launch_fused_gr<F32, F32>(dr, p, s);
+    if (gdtype == 1 && rdtype == 1) blocks = launch_fused_gr<BF16, BF16>(dr, p, h, s);
+    else if (gdtype == 1) blocks = launch_fused_gr<BF16, F32>(dr, p, h, s);
+    else if (rdtype == 1) blocks = launch_fused_gr<F32, BF16>(dr, p, h, s);
+    else blocks = launch_fused_gr<F32, F32>(dr, p, h, s);
+    if (blocks < 0) return hipErrorLaunchFailure;
     hipError_t e = hipGetLastError();
     if (e != hipSuccess || !dr) return e;
     return launch_drift_reduce(p.partials, blocks, p.groups, p.n, p.d, 1, drift, s);

@@ -90,37 +90,79 @@ __device__ __forceinline__ uint32_t f32_to_bf16(float f) {
     return (u + 0x7FFFu + ((u >> 16) & 1u)) >> 16;
 }
 
-// Load 8 consecutive elements (16-byte aligned when full) as floats.
+// Memory access of a thread's 8 consecutive elements.  Kernels decide per
+// tile (wave-uniformly) which of two forms every access of the tile takes:
+//   W = true   every thread of the tile owns 0 or 8 elements and the tile
+//              starts on a 16-byte boundary: one 16-byte access per 8 bf16
+//              (two per 8 fp32), predicated on nv == 8.  Loads land in raw
+//              registers and are unpacked only when used, so a batch of row
+//              loads is in flight together.
+//   W = false  element by element (a shard end that is not a multiple of 8,
+//              or packets whose length is not a multiple of 8 elements).
+// Raw storage of 8 consecutive elements.
 template <class E>
-__device__ __forceinline__ void load8(const typename E::T* p, int nv, float (&x)[8]);
-
+struct Raw8;
 template <>
-__device__ __forceinline__ void load8<F32>(const float* p, int nv, float (&x)[8]) {
-    if (nv == 8) {
-        const u32x4 a = *reinterpret_cast<const u32x4*>(p);
-        const u32x4 b = *reinterpret_cast<const u32x4*>(p + 4);
-        x[0] = __uint_as_float(a.x); x[1] = __uint_as_float(a.y);
-        x[2] = __uint_as_float(a.z); x[3] = __uint_as_float(a.w);
-        x[4] = __uint_as_float(b.x); x[5] = __uint_as_float(b.y);
-        x[6] = __uint_as_float(b.z); x[7] = __uint_as_float(b.w);
+struct Raw8<F32> {
+    u32x4 a, b;
+};
+template <>
+struct Raw8<BF16> {
+    u32x4 a;
+};
+
+template <bool W>
+__device__ __forceinline__ void load_raw(const float* p, int nv, Raw8<F32>& r) {
+    r.a = u32x4{0, 0, 0, 0};
+    r.b = u32x4{0, 0, 0, 0};
+    if (W) {
+        if (nv == 8) {
+            r.a = *reinterpret_cast<const u32x4*>(p);
+            r.b = *reinterpret_cast<const u32x4*>(p + 4);
+        }
     } else {
+        uint32_t w[8];
 #pragma unroll
-        for (int j = 0; j < 8; ++j) x[j] = j < nv ? p[j] : 0.0f;
+        for (int j = 0; j < 8; ++j) w[j] = j < nv ? __float_as_uint(p[j]) : 0u;
+        r.a = u32x4{w[0], w[1], w[2], w[3]};
+        r.b = u32x4{w[4], w[5], w[6], w[7]};
     }
 }
 
-template <>
-__device__ __forceinline__ void load8<BF16>(const uint16_t* p, int nv, float (&x)[8]) {
-    if (nv == 8) {
-        const u32x4 a = *reinterpret_cast<const u32x4*>(p);
-        x[0] = bf16_to_f32(a.x & 0xFFFFu); x[1] = bf16_to_f32(a.x >> 16);
-        x[2] = bf16_to_f32(a.y & 0xFFFFu); x[3] = bf16_to_f32(a.y >> 16);
-        x[4] = bf16_to_f32(a.z & 0xFFFFu); x[5] = bf16_to_f32(a.z >> 16);
-        x[6] = bf16_to_f32(a.w & 0xFFFFu); x[7] = bf16_to_f32(a.w >> 16);
+template <bool W>
+__device__ __forceinline__ void load_raw(const uint16_t* p, int nv, Raw8<BF16>& r) {
+    r.a = u32x4{0, 0, 0, 0};
+    if (W) {
+        if (nv == 8) r.a = *reinterpret_cast<const u32x4*>(p);
     } else {
+        uint32_t w[4] = {0, 0, 0, 0};
 #pragma unroll
-        for (int j = 0; j < 8; ++j) x[j] = j < nv ? bf16_to_f32(p[j]) : 0.0f;
+        for (int j = 0; j < 8; ++j)
+            if (j < nv) w[j >> 1] |= (uint32_t)p[j] << (16 * (j & 1));
+        r.a = u32x4{w[0], w[1], w[2], w[3]};
     }
+}
+
+__device__ __forceinline__ void unpack(const Raw8<F32>& r, float (&x)[8]) {
+    x[0] = __uint_as_float(r.a.x); x[1] = __uint_as_float(r.a.y);
+    x[2] = __uint_as_float(r.a.z); x[3] = __uint_as_float(r.a.w);
+    x[4] = __uint_as_float(r.b.x); x[5] = __uint_as_float(r.b.y);
+    x[6] = __uint_as_float(r.b.z); x[7] = __uint_as_float(r.b.w);
+}
+
+__device__ __forceinline__ void unpack(const Raw8<BF16>& r, float (&x)[8]) {
+    x[0] = bf16_to_f32(r.a.x & 0xFFFFu); x[1] = bf16_to_f32(r.a.x >> 16);
+    x[2] = bf16_to_f32(r.a.y & 0xFFFFu); x[3] = bf16_to_f32(r.a.y >> 16);
+    x[4] = bf16_to_f32(r.a.z & 0xFFFFu); x[5] = bf16_to_f32(r.a.z >> 16);
+    x[6] = bf16_to_f32(r.a.w & 0xFFFFu); x[7] = bf16_to_f32(r.a.w >> 16);
+}
+
+// 8 consecutive elements as floats (0 past nv).
+template <class E, bool W>
+__device__ __forceinline__ void load8(const typename E::T* p, int nv, float (&x)[8]) {
+    Raw8<E> r;
+    load_raw<W>(p, nv, r);
+    unpack(r, x);
 }
 
 // Rounded storage form of 8 values (what a replica row holds).
@@ -129,22 +171,25 @@ struct Packed8;
 
 template <>
 struct Packed8<F32> {
-    u32x4 a, b;
+    Raw8<F32> r;
     __device__ __forceinline__ void pack(const float (&x)[8]) {
-        a = u32x4{__float_as_uint(x[0]), __float_as_uint(x[1]), __float_as_uint(x[2]),
-                  __float_as_uint(x[3])};
-        b = u32x4{__float_as_uint(x[4]), __float_as_uint(x[5]), __float_as_uint(x[6]),
-                  __float_as_uint(x[7])};
+        r.a = u32x4{__float_as_uint(x[0]), __float_as_uint(x[1]), __float_as_uint(x[2]),
+                    __float_as_uint(x[3])};
+        r.b = u32x4{__float_as_uint(x[4]), __float_as_uint(x[5]), __float_as_uint(x[6]),
+                    __float_as_uint(x[7])};
     }
     __device__ __forceinline__ float value(int j) const {
-        const u32x4& h = j < 4 ? a : b;
+        const u32x4& h = j < 4 ? r.a : r.b;
         const int q = j & 3;
         return __uint_as_float(q == 0 ? h.x : q == 1 ? h.y : q == 2 ? h.z : h.w);
     }
+    template <bool W>
     __device__ __forceinline__ void store(float* p, int nv) const {
-        if (nv == 8) {
-            __builtin_nontemporal_store(a, reinterpret_cast<u32x4*>(p));
-            __builtin_nontemporal_store(b, reinterpret_cast<u32x4*>(p + 4));
+        if (W) {
+            if (nv == 8) {
+                __builtin_nontemporal_store(r.a, reinterpret_cast<u32x4*>(p));
+                __builtin_nontemporal_store(r.b, reinterpret_cast<u32x4*>(p + 4));
+            }
         } else {
             for (int j = 0; j < nv; ++j) p[j] = value(j);
         }
@@ -153,39 +198,63 @@ struct Packed8<F32> {
 
 template <>
 struct Packed8<BF16> {
-    u32x4 a;
+    Raw8<BF16> r;
     __device__ __forceinline__ void pack(const float (&x)[8]) {
-        a = u32x4{f32_to_bf16(x[0]) | (f32_to_bf16(x[1]) << 16),
-                  f32_to_bf16(x[2]) | (f32_to_bf16(x[3]) << 16),
-                  f32_to_bf16(x[4]) | (f32_to_bf16(x[5]) << 16),
-                  f32_to_bf16(x[6]) | (f32_to_bf16(x[7]) << 16)};
+        r.a = u32x4{f32_to_bf16(x[0]) | (f32_to_bf16(x[1]) << 16),
+                    f32_to_bf16(x[2]) | (f32_to_bf16(x[3]) << 16),
+                    f32_to_bf16(x[4]) | (f32_to_bf16(x[5]) << 16),
+                    f32_to_bf16(x[6]) | (f32_to_bf16(x[7]) << 16)};
     }
     __device__ __forceinline__ float value(int j) const {
         const int q = j >> 1;
-        const uint32_t w = q == 0 ? a.x : q == 1 ? a.y : q == 2 ? a.z : a.w;
+        const uint32_t w = q == 0 ? r.a.x : q == 1 ? r.a.y : q == 2 ? r.a.z : r.a.w;
         return bf16_to_f32((j & 1) ? (w >> 16) : (w & 0xFFFFu));
     }
+    template <bool W>
     __device__ __forceinline__ void store(uint16_t* p, int nv) const {
-        if (nv == 8) {
-            __builtin_nontemporal_store(a, reinterpret_cast<u32x4*>(p));
+        if (W) {
+            if (nv == 8) __builtin_nontemporal_store(r.a, reinterpret_cast<u32x4*>(p));
         } else {
             for (int j = 0; j < nv; ++j) p[j] = (uint16_t)f32_to_bf16(value(j));
         }
     }
 };
 
-__device__ __forceinline__ void load_f32x8(const float* p, int nv, float (&x)[8]) {
-    load8<F32>(p, nv, x);
-}
-
+template <bool W>
 __device__ __forceinline__ void store_f32x8(float* p, int nv, const float (&x)[8]) {
-    if (nv == 8) {
-        *reinterpret_cast<u32x4*>(p) = u32x4{__float_as_uint(x[0]), __float_as_uint(x[1]),
-                                             __float_as_uint(x[2]), __float_as_uint(x[3])};
-        *reinterpret_cast<u32x4*>(p + 4) = u32x4{__float_as_uint(x[4]), __float_as_uint(x[5]),
-                                                 __float_as_uint(x[6]), __float_as_uint(x[7])};
+    if (W) {
+        if (nv == 8) {
+            *reinterpret_cast<u32x4*>(p) = u32x4{__float_as_uint(x[0]), __float_as_uint(x[1]),
+                                                 __float_as_uint(x[2]), __float_as_uint(x[3])};
+            *reinterpret_cast<u32x4*>(p + 4) = u32x4{__float_as_uint(x[4]), __float_as_uint(x[5]),
+                                                     __float_as_uint(x[6]), __float_as_uint(x[7])};
+        }
     } else {
         for (int j = 0; j < nv; ++j) p[j] = x[j];
+    }
+}
+
+// Store raw storage back bit for bit (16-byte non-temporal stores when W).
+template <bool W>
+__device__ __forceinline__ void store_raw(float* p, int nv, const Raw8<F32>& r) {
+    if (W) {
+        if (nv == 8) {
+            __builtin_nontemporal_store(r.a, reinterpret_cast<u32x4*>(p));
+            __builtin_nontemporal_store(r.b, reinterpret_cast<u32x4*>(p + 4));
+        }
+    } else {
+        const uint32_t w[8] = {r.a.x, r.a.y, r.a.z, r.a.w, r.b.x, r.b.y, r.b.z, r.b.w};
+        for (int j = 0; j < nv; ++j) p[j] = __uint_as_float(w[j]);
+    }
+}
+
+template <bool W>
+__device__ __forceinline__ void store_raw(uint16_t* p, int nv, const Raw8<BF16>& r) {
+    if (W) {
+        if (nv == 8) __builtin_nontemporal_store(r.a, reinterpret_cast<u32x4*>(p));
+    } else {
+        const uint32_t w[4] = {r.a.x, r.a.y, r.a.z, r.a.w};
+        for (int j = 0; j < nv; ++j) p[j] = (uint16_t)(w[j >> 1] >> (16 * (j & 1)));
     }
 }
 
@@ -250,6 +319,46 @@ __device__ __forceinline__ int popcount_words(const uint64_t* words, int nw) {
 }
 
 // ---------------------------------------------------------------------------
+// Row pacing.  Workgroups that stream many rows at the same column offset
+// reach the HBM much faster when all of them touch the same row at the same
+// time (a few concurrent row streams instead of one per row).  A paced kernel
+// therefore issues the access of row i of a phase no earlier than a slot time
+// read from the constant-rate 100 MHz clock that every compute unit sees; the
+// schedule only delays accesses, so results never depend on it.
+// ---------------------------------------------------------------------------
+__device__ __forceinline__ uint64_t clock_ticks() { return __builtin_amdgcn_s_memrealtime(); }
+
+// Accessors without pacing (one-stage kernels and the unpaced fused step).
+struct NoPace {
+    __device__ __forceinline__ void grad(int) const {}
+    __device__ __forceinline__ void rep(int) const {}
+    __device__ __forceinline__ void stale(int) const {}
+};
+
+// Slot times of one round of a paced kernel, in 1/256 clock ticks: the
+// access of row i in the gradient, replica and stale-read sweeps waits for
+// base + off + i * delta of that sweep.  A slot further away than `guard`
+// ticks (a stale or foreign anchor) is not waited for, so every wait ends.
+struct ClockPace {
+    uint64_t base;  // round start, ticks
+    uint64_t off_g, off_r, off_s;  // sweep starts, 1/256 ticks after base
+    uint64_t dg, dr, ds;           // slot lengths, 1/256 ticks
+    uint64_t guard;                // ticks
+    __device__ __forceinline__ void at(uint64_t off, uint64_t delta, int i) const {
+        const uint64_t t = base + ((off + (uint64_t)i * delta) >> 8);
+        uint64_t now = clock_ticks();
+        if (t <= now || t - now > guard) return;
+        while (now < t) {
+            __builtin_amdgcn_s_sleep(1);
+            now = clock_ticks();
+        }
+    }
+    __device__ __forceinline__ void grad(int i) const { at(off_g, dg, i); }
+    __device__ __forceinline__ void rep(int i) const { at(off_r, dr, i); }
+    __device__ __forceinline__ void stale(int i) const { at(off_s, ds, i); }
+};
+
+// ---------------------------------------------------------------------------
 // Aggregate of one packet's contributions, 8 elements per thread.
 // ---------------------------------------------------------------------------
 enum { kEstArrivedMean = 0, kEstHorvitzThompson = 1, kEstStaleFill = 2 };
@@ -304,36 +413,35 @@ __device__ __forceinline__ float parity_invq(const AggVariant& v, int64_t k, int
 // Stale fill (Algorithm 1): every row in ascending order contributes its
 // arrived value or, if lost, its last arrived one from g_prev; arrived values
 // are written to g_prev; g = sum / n.
-template <class E>
+template <class E, bool W, class Pace>
 __device__ __forceinline__ void aggregate8(const typename E::T* grads, int64_t ld,
                                            int64_t e0, int nv, const uint64_t* gm, int nw,
                                            int n, int K, float lam, const float (&th)[8],
                                            const AggVariant& var, bool reliable_packet,
-                                           float (&g)[8]) {
+                                           const Pace& pace, float (&g)[8]) {
 #pragma unroll
     for (int j = 0; j < 8; ++j) g[j] = 0.0f;
     if (var.kind == kEstStaleFill) {
         typename E::T* prev = reinterpret_cast<typename E::T*>(var.g_prev);
         for (int i0 = 0; i0 < n; i0 += kBatchGrad) {
-            float x[kBatchGrad][8];
+            Raw8<E> raw[kBatchGrad];
             bool arr[kBatchGrad];
 #pragma unroll
             for (int u = 0; u < kBatchGrad; ++u) {
                 const int row = i0 + u < n ? i0 + u : i0;
                 arr[u] = (uniform64(gm[row >> 6]) >> (row & 63)) & 1;
                 const typename E::T* src = arr[u] ? grads : prev;
-                load8<E>(src + (int64_t)row * ld + e0, nv, x[u]);
+                pace.grad(row);
+                load_raw<W>(src + (int64_t)row * ld + e0, nv, raw[u]);
             }
 #pragma unroll
             for (int u = 0; u < kBatchGrad; ++u) {
                 if (i0 + u < n) {
+                    float x[8];
+                    unpack(raw[u], x);
 #pragma unroll
-                    for (int j = 0; j < 8; ++j) g[j] += x[u][j];
-                    if (arr[u]) {
-                        Packed8<E> keep;
-                        keep.pack(x[u]);
-                        keep.store(prev + (int64_t)(i0 + u) * ld + e0, nv);
-                    }
+                    for (int j = 0; j < 8; ++j) g[j] += x[j];
+                    if (arr[u]) store_raw<W>(prev + (int64_t)(i0 + u) * ld + e0, nv, raw[u]);
                 }
             }
         }
@@ -354,17 +462,20 @@ __device__ __forceinline__ void aggregate8(const typename E::T* grads, int64_t l
                 idx[u] = bits ? (w * 64 + __builtin_ctzll(bits)) : -1;
                 bits &= bits - 1;  // no-op once bits == 0
             }
-            float x[kBatchGrad][8];
+            Raw8<E> raw[kBatchGrad];
 #pragma unroll
             for (int u = 0; u < kBatchGrad; ++u) {
                 const int row = idx[u] >= 0 ? idx[u] : idx[0];
-                load8<E>(grads + (int64_t)row * ld + e0, nv, x[u]);
+                pace.grad(row);
+                load_raw<W>(grads + (int64_t)row * ld + e0, nv, raw[u]);
             }
 #pragma unroll
             for (int u = 0; u < kBatchGrad; ++u) {
                 if (idx[u] >= 0) {
+                    float x[8];
+                    unpack(raw[u], x);
 #pragma unroll
-                    for (int j = 0; j < 8; ++j) g[j] += x[u][j];
+                    for (int j = 0; j < 8; ++j) g[j] += x[j];
                 }
             }
         }
@@ -376,7 +487,10 @@ __device__ __forceinline__ void aggregate8(const typename E::T* grads, int64_t l
             for (int j = 0; j < 8; ++j) g[j] = g[j] / nf;
         } else {
             float own[8] = {0, 0, 0, 0, 0, 0, 0, 0};
-            if (sure_row >= 0) load8<E>(grads + (int64_t)sure_row * ld + e0, nv, own);
+            if (sure_row >= 0) {
+                pace.grad(sure_row);
+                load8<E, W>(grads + (int64_t)sure_row * ld + e0, nv, own);
+            }
 #pragma unroll
             for (int j = 0; j < 8; ++j) g[j] = (g[j] * var.invq + own[j]) / nf;
         }
@@ -455,7 +569,9 @@ struct Drift8 {
             }
         }
     }
-    // Fold into per-thread totals: pair sum N*S2 - S1^2 and max range.
+    // Fold into per-thread totals: pair sum N*S2 - S1^2 per element (clamped
+    // at 0 against rounding, so that identical rows give exactly 0) and the
+    // max range.
     __device__ __forceinline__ void finish(int n, int nv, double& pair, double& range) const {
 #pragma unroll
         for (int j = 0; j < 8; ++j) {

@@ -22,7 +22,8 @@ def test_header_declares_the_boundary():
     names = set(_declared())
     assert names == {"ll_masks", "lossy_aggregate", "shard_step", "lossy_broadcast",
                      "drift_stats", "lossy_step_fused", "ll_workspace_bytes",
-                     "ll_masks_workspace_bytes", "ll_ages_update", "ll_last_error"}
+                     "ll_masks_workspace_bytes", "ll_ages_update", "ll_last_error",
+                     "ll_set_pacing", "ll_get_pacing"}
 
 
 def test_library_exports_every_declared_symbol():
@@ -61,7 +62,10 @@ def test_workspace_bytes_host_logic():
     assert ll.ll_masks_workspace_bytes(16, 65536) == ge(16, 65536)
     assert ll.ll_masks_workspace_bytes(0, 5) == 0
     assert ll.ll_workspace_bytes(0, 10, 8) == 0      # invalid n
-    assert ll.ll_workspace_bytes(4, 10, 12) == 0     # packet not a multiple of 8
+    assert ll.ll_workspace_bytes(4, 10, 0) == 0      # packet < 1
+    # any packet length >= 1: P = ceil(d / L), one partial per chunk of 1024
+    assert ll.ll_workspace_bytes(4, 10, 3) == r256(4 * 32) + groups + 2 * 256 + 2 * ge(4, 4)
+    assert ll.ll_workspace_bytes(4, 10, 12) == 256 + groups + 2 * 256 + 2 * ge(4, 1)
     assert ll.ll_workspace_bytes(4, -1, 8) == 0
 
 
@@ -73,11 +77,14 @@ def _raw():
     ((0, 16, 8, 0, 16, 16, 0, 0.0, 0, 16, 0, 0), -1, "n=0"),
     ((2000, 16, 8, 0, 16, 16, 0, 0.0, 0, 16, 0, 0), -1, "n=2000"),
     ((2, -5, 8, 0, 16, 16, 16, 0.0, 0, 16, 0, 0), -1, "negative"),
-    ((2, 16, 12, 0, 16, 16, 16, 0.0, 0, 16, 0, 0), -1, "multiple of 8"),
+    ((2, 16, 0, 0, 16, 16, 16, 0.0, 0, 16, 0, 0), -1, "packet=0 must be at least 1"),
+    ((2, 16, -3, 0, 16, 16, 16, 0.0, 0, 16, 0, 0), -1, "at least 1"),
     ((2, 16, 8, 7, 16, 16, 16, 0.0, 0, 16, 0, 0), -1, "dtype"),
     ((2, 16, 8, 0, 0, 16, 16, 0.0, 0, 16, 0, 0), -1, "grads is NULL"),
     ((2, 16, 8, 0, 16, 8, 16, 0.0, 0, 16, 0, 0), -1, "ld=8 < d=16"),
-    ((2, 16, 8, 0, 16, 20, 16, 0.0, 0, 16, 0, 0), -2, "multiple of 8"),
+    # fp32 rows need ld a multiple of 4 elements, bf16 rows a multiple of 8
+    ((2, 16, 8, 0, 16, 18, 16, 0.0, 0, 16, 0, 0), -2, "not a multiple of 16 bytes"),
+    ((2, 16, 8, 1, 16, 20, 16, 0.0, 0, 16, 0, 0), -2, "ld=20 elements of 2 bytes"),
     ((2, 16, 8, 0, 18, 16, 16, 0.0, 0, 16, 0, 0), -2, "aligned"),
     ((2, 16, 8, 0, 16, 16, 0, 0.0, 0, 16, 0, 0), -1, "arrived is NULL"),
     ((2, 16, 8, 0, 16, 16, 16, 0.5, 0, 16, 0, 0), -1, "theta is NULL"),
@@ -228,3 +235,29 @@ def test_missing_library_fails_loudly(monkeypatch):
         ll.ll_workspace_bytes(4, 100, 8)
     with pytest.raises(RuntimeError, match="not built"):
         ll.ll_last_error()
+
+
+def test_pacing_setting_round_trips_and_rejects_bad_values():
+    before = ll.ll_get_pacing()
+    try:
+        want = dict(mode="never", bytes_per_s=5.0e12, gap_us=1.5, lead_us=3.0, overlap=1,
+                    resident=2, headroom=0.75)
+        ll.ll_set_pacing(**want)
+        assert ll.ll_get_pacing() == want
+        for bad in ((0.0, 1.0, 1.0, 2, 3), (-1.0, 1.0, 1.0, 2, 3), (2e15, 1.0, 1.0, 2, 3),
+                    (6e12, -1.0, 1.0, 2, 3), (6e12, 2e4, 1.0, 2, 3), (6e12, 1.0, -1.0, 2, 3),
+                    (6e12, 1.0, 1.0, 0, 3), (6e12, 1.0, 1.0, 3, 3), (6e12, 1.0, 1.0, 2, 1),
+                    (6e12, 1.0, 1.0, 1, 5), (6e12, 1.0, 1.0, 1, 1, 0.0), (6e12, 1.0, 1.0, 1, 1, 1.5)):
+            with pytest.raises(ll.LossyError):
+                ll.ll_set_pacing("auto", *bad)
+        lib = _raw()
+        lib.ll_set_pacing.argtypes = [ctypes.c_void_p]
+        lib.ll_last_error.restype = ctypes.c_char_p
+        cfg = ll.Pacing(7, 6e12, 2.0, 2.5, 2, 2, 0.9)
+        assert lib.ll_set_pacing(ctypes.byref(cfg)) == -1
+        assert "unknown pacing mode 7" in lib.ll_last_error().decode()
+        assert lib.ll_set_pacing(None) == -1
+        # a rejected setting leaves the previous one in place
+        assert ll.ll_get_pacing() == want
+    finally:
+        ll.ll_set_pacing(**before)
