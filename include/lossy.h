@@ -328,22 +328,28 @@ LL_API int lossy_step_fused(int32_t n, int64_t d, int64_t packet, uint64_t step,
  * step runs at the set rate.
  *   mode         LL_PACE_AUTO (default): paced when the step spans at least 8
  *                rounds; LL_PACE_ALWAYS; LL_PACE_NEVER.
- *   bytes_per_s  rate the slots are laid out for (default 6.0e12).
+ *   bytes_per_s  rate the slots are laid out for (default 6.25e12).
  *   gap_us       time between the last gradient slot and the first replica
  *                slot, besides the master and moment writes (default 2).
  *   lead_us      time from a round's start to its first gradient slot,
- *                besides the master and moment reads (default 2.5).
- *   overlap      rounds streaming at once (1 or 2; default 2): with 2, each
- *                round gets half the rate and rounds start half a round
- *                apart, so one round's gradient sweep runs beside the
- *                previous round's replica sweep and each round's lead and gap
- *                are covered by the other's streams.
+ *                besides the master and moment reads (default 4).
+ *   overlap      rounds streaming at once (1 or 2; default 1).  With 1,
+ *                rounds run back to back and the chip streams one row at a
+ *                time, reading in the gradient sweep and writing in the
+ *                replica sweep.  With 2, each round gets half the rate and
+ *                rounds start half a round apart, so one round's gradient
+ *                sweep runs beside the previous round's replica sweep and
+ *                each round's lead and gap are covered by the other's
+ *                streams (two mixed streams: measured to hold about 6.0e12).
  *   resident     rounds sharing the workgroup places the chip holds at once
- *                (overlap..4; default 2): a round has headroom / resident of
+ *                (overlap..4; default 1): a round has headroom / resident of
  *                them, and rounds start no closer than a round's length /
  *                resident apart, so that every round's workgroups find places
  *                when it starts.
  *   headroom     fraction of those places the rounds fill ((0, 1]; 0.9).
+ * A workgroup that starts more than 10 us behind its round (its place freed
+ * late) keeps the round's pace from its own start rather than rushing
+ * through the slots it missed; smaller lateness is caught up.
  * The setting is process-wide and read at each call.  A paced step enqueues,
  * before the step itself: the Bernoulli mask kernel for each direction whose
  * masks have memory to go to (the caller's mask output, else the workspace

@@ -232,8 +232,8 @@ class Pacing(ctypes.Structure):
 PACE_MODES = {"auto": 0, "always": 1, "never": 2}
 
 
-def ll_set_pacing(mode: str = "auto", bytes_per_s: float = 6.0e12, gap_us: float = 2.0,
-                  lead_us: float = 2.5, overlap: int = 2, resident: int = 2,
+def ll_set_pacing(mode: str = "auto", bytes_per_s: float = 6.25e12, gap_us: float = 2.0,
+                  lead_us: float = 4.0, overlap: int = 1, resident: int = 1,
                   headroom: float = 0.9) -> None:
     """Process-wide pacing of lossy_step_fused (a performance setting; see
     include/lossy.h)."""

@@ -142,6 +142,8 @@ struct PaceParams {
     uint64_t off_g, off_r, off_s;  // gradient, replica and stale-read sweep starts
     uint64_t dg, dr, ds;           // slot lengths of the three sweeps
     uint64_t guard;                // longest wait, ticks
+    uint64_t lead;                 // lead of a round, ticks
+    uint64_t late;                 // lateness past which a workgroup keeps its own pace, ticks
 };
 
 // Pacing modes and defaults: auto paces steps of at least kPaceMinRounds
@@ -150,12 +152,15 @@ struct PaceParams {
 // kPaceMarginUs after the anchor is written.
 enum { kPaceAuto = 0, kPaceAlways = 1, kPaceNever = 2 };
 constexpr int64_t kPaceMinRounds = 8;
-constexpr double kDefaultPaceRate = 6.0e12;
+constexpr double kDefaultPaceRate = 6.25e12;
 constexpr double kDefaultPaceGapUs = 2.0;
-constexpr double kDefaultPaceLeadUs = 2.5;
-constexpr int kDefaultPaceOverlap = 2;
-constexpr int kDefaultPaceResident = 2;
+constexpr double kDefaultPaceLeadUs = 4.0;
+constexpr int kDefaultPaceOverlap = 1;
+constexpr int kDefaultPaceResident = 1;
 constexpr double kPaceMarginUs = 5.0;
+constexpr double kPaceTailUs = 2.5;
+// Lateness past which a workgroup keeps its round's pace from its own start.
+constexpr double kPaceLateUs = 10.0;
 // Fraction of the resident workgroup places the rounds in flight may fill.
 constexpr double kDefaultPaceHeadroom = 0.9;
 

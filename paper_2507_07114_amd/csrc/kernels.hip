@@ -639,11 +639,20 @@ __global__ void k_pace_anchor(uint64_t margin_ticks) {
 template <class G, class R, bool DRIFT>
 __global__ __launch_bounds__(R::kPacketThreads) void k_step_paced(FusedParams p, PaceParams q) {
     __shared__ uint64_t s_words[2][kMaxWords];
+    __shared__ uint64_t s_entry;
+    if (threadIdx.x == 0) s_entry = clock_ticks();
     const uint64_t t0 =
         __hip_atomic_load(&g_pace_anchor, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     const uint64_t r = (uint64_t)blockIdx.x / (uint64_t)q.per_round;
+    __syncthreads();
     ClockPace pace;
-    pace.base = t0 + ((r * q.round) >> 8);
+    // A workgroup that starts far behind its round (its place freed late,
+    // by more than q.late) keeps the round's pace from its own start instead
+    // of rushing through the slots it missed, so that badly late workgroups
+    // stay in step with each other; smaller lateness is caught up.
+    const uint64_t nominal = t0 + ((r * q.round) >> 8);
+    const uint64_t entry = s_entry;
+    pace.base = (entry > nominal + q.late && entry - nominal < q.guard) ? entry - q.lead : nominal;
     pace.off_g = q.off_g;
     pace.off_r = q.off_r;
     pace.off_s = q.off_s;
@@ -879,7 +888,9 @@ static bool pace_plan(const FusedParams& p, const PaceHint& h, int64_t tiles, Pa
     const double off_g = st.lead_us * us + g * state * fp;
     const double off_r = off_g + n * dg + g * state * fp + st.gap_us * us;
     const double off_s = off_r + n * dr;
-    const double length = off_s + n * ds;
+    // A round's workgroups leave a little after its last slot: the last rows
+    // they read must arrive and the drift partial be folded.
+    const double length = off_s + n * ds + kPaceTailUs * us;
     // Rounds start `spacing` apart: no closer than the round's bytes at its
     // share allow with k rounds streaming (stream / k), and far enough apart
     // that a round's workgroups find places when it starts, res rounds
@@ -890,6 +901,8 @@ static bool pace_plan(const FusedParams& p, const PaceHint& h, int64_t tiles, Pa
     const double spacing = stream / k > length / res ? stream / k : length / res;
     if (!(length < 1e15)) return false;
     q->per_round = g;
+    q->lead = (uint64_t)(st.lead_us * 1e-6 * tick_hz);
+    q->late = (uint64_t)(kPaceLateUs * 1e-6 * tick_hz);
     q->dg = (uint64_t)dg;
     q->dr = (uint64_t)dr;
     q->ds = (uint64_t)ds;
