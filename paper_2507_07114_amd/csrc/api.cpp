@@ -176,7 +176,7 @@ struct WsLayout {
 WsLayout ws_layout(int32_t n, const Geometry& g) {
     WsLayout w;
     w.groups_off = round256((size_t)g.blocks * sizeof(DriftPartial));
-    w.partials = w.groups_off + round256((size_t)kReduceGroups * sizeof(DriftAcc));
+    w.partials = w.groups_off + round256(kReduceBytes);
     w.masks = round256((size_t)n * (size_t)g.P);
     w.gs = ge_scratch(n, g.P);
     w.ge = 2 * w.gs.per_dir;
@@ -230,7 +230,7 @@ int make_parity(const ExtView& x, int32_t n, int64_t P, uint64_t step, ParityLau
 
 void add_parity_job(ParityLaunch* L, const ll_loss* l, int dir, const ExtView& x,
                     uint8_t* arrived) {
-    ParityJob& j = L->job[L->ndir++];
+    MaskJob& j = L->job[L->ndir++];
     j.dir = (uint64_t)dir;
     j.seed = l->seed;
     j.thr = threshold(l->p);

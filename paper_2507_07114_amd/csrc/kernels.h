@@ -46,6 +46,13 @@ struct GeParams {
 // Workgroups of the first drift reduction level.
 constexpr int kReduceGroups = 256;
 
+// The second-level partials are followed by the counter with which the last
+// reducing workgroup finds itself.
+__host__ __device__ inline unsigned* reduce_counter(DriftAcc* groups) {
+    return reinterpret_cast<unsigned*>(groups + kReduceGroups);
+}
+constexpr size_t kReduceBytes = kReduceGroups * sizeof(DriftAcc) + 16;
+
 // Gilbert-Elliott scan geometry: a thread composes kGeRun consecutive packets,
 // a workgroup one segment of kGeSeg packets.
 constexpr int kGeRun = 16;
@@ -104,7 +111,7 @@ struct DriftParams {
     const float* theta;
     const uint8_t* arrived;
     DriftPartial* partials;
-    DriftAcc* groups;  // [kReduceGroups] second-level partials
+    DriftAcc* groups;  // [kReduceGroups] second-level partials, then the counter
 };
 
 struct FusedParams {
@@ -126,7 +133,7 @@ struct FusedParams {
     void* replicas;
     int64_t ld_r;
     DriftPartial* partials;
-    DriftAcc* groups;  // [kReduceGroups] second-level partials
+    DriftAcc* groups;  // [kReduceGroups] second-level partials, then the counter
     AggVariant var;
     uint16_t* ages;    // [n][P] broadcast ages, or null
     // [n][P] memory where a paced step may draw each direction's Bernoulli
@@ -157,7 +164,7 @@ constexpr double kDefaultPaceGapUs = 2.0;
 constexpr double kDefaultPaceLeadUs = 4.0;
 constexpr int kDefaultPaceOverlap = 1;
 constexpr int kDefaultPaceResident = 1;
-constexpr double kPaceMarginUs = 5.0;
+constexpr double kPaceMarginUs = 3.0;
 constexpr double kPaceTailUs = 2.5;
 // Lateness past which a workgroup keeps its round's pace from its own start.
 constexpr double kPaceLateUs = 10.0;
@@ -185,8 +192,8 @@ struct PaceHint {
 // Largest packet group of the parity-packet recovery.
 constexpr int kMaxParityGroup = 256;
 
-// One direction's Bernoulli masks with parity recovery.
-struct ParityJob {
+// One direction's Bernoulli masks (with parity recovery in k_masks_parity).
+struct MaskJob {
     uint64_t dir, seed, thr;
     int owner;
     const uint8_t* reliable;  // [P] or null
@@ -199,10 +206,12 @@ struct ParityLaunch {
     int ndir, n, G, span;
     int64_t P, spans;  // spans = ceil(P / span) per row
     uint64_t step;
-    ParityJob job[2];
+    MaskJob job[2];
 };
 
 hipError_t launch_masks_parity(const ParityLaunch& L, hipStream_t s);
+hipError_t launch_masks_bernoulli_jobs(int n, int64_t num_packets, uint64_t step,
+                                       const MaskJob* jobs, int njobs, hipStream_t s);
 hipError_t launch_masks_bernoulli(int n, int64_t num_packets, uint64_t step, int dir,
                                   uint64_t seed, uint64_t thr, int owner,
                                   const uint8_t* reliable, uint8_t* arrived, hipStream_t s);

@@ -40,6 +40,30 @@ __global__ __launch_bounds__(kThreads) void k_masks_bernoulli(int n, int64_t num
     }
 }
 
+// Bernoulli masks of one or two directions in one launch (job j covers
+// entries [j n P, (j + 1) n P) of the grid).
+struct MaskJobs {
+    MaskJob job[2];
+};
+
+__global__ __launch_bounds__(kThreads) void k_masks_bernoulli_jobs(int n, int64_t num_packets,
+                                                                   uint64_t step, int njobs,
+                                                                   MaskJobs J) {
+    const int64_t per = (int64_t)n * num_packets;
+    const int64_t total = per * njobs;
+    for (int64_t idx = (int64_t)blockIdx.x * kThreads + threadIdx.x; idx < total;
+         idx += (int64_t)gridDim.x * kThreads) {
+        const int j = idx >= per ? 1 : 0;
+        const MaskJob& m = J.job[j];
+        const int64_t e = idx - j * per;
+        const int64_t i = e / num_packets;
+        const int64_t k = e - i * num_packets;
+        const bool a = bernoulli_arrived((uint64_t)k, (uint64_t)i, step, m.dir, m.seed, m.thr) ||
+                       forced_arrival((int)i, k, m.owner, m.reliable);
+        m.arrived[e] = a ? 1 : 0;
+    }
+}
+
 // Bernoulli masks with parity packets.  A workgroup takes `span` consecutive
 // packets of one (direction, row), one packet per thread, span a multiple of
 // G.  Each thread draws its packet's arrival and applies the transfers that
@@ -54,7 +78,7 @@ __global__ __launch_bounds__(kThreads) void k_masks_parity(ParityLaunch L) {
     const int64_t per_dir = (int64_t)L.n * L.spans;
     const int64_t b = blockIdx.x;
     const int s = b >= per_dir ? 1 : 0;
-    const ParityJob& J = L.job[s];
+    const MaskJob& J = L.job[s];
     const int64_t rem = b - s * per_dir;
     const int64_t i = rem / L.spans;
     const int64_t k0 = (rem - i * L.spans) * L.span;
@@ -382,11 +406,11 @@ __global__ __launch_bounds__(R::kPacketThreads) void k_drift(DriftParams p) {
         else drift_chunk<R, false>(p, ch, pair, range, abs_sum);
     }
     block_reduce_partial<NT>(pair, abs_sum, range, stale, 0, p.partials + blockIdx.x);
+    if (blockIdx.x == 0 && threadIdx.x == 0) *reduce_counter(p.groups) = 0u;
 }
 
 // Fixed-order reduction of the per-workgroup partials into the ll_drift
-// record, in two launches: kReduceGroups workgroups each fold a contiguous
-// range of partials, then one workgroup folds those and writes the record.
+// record.
 // Fixed-order tree over the workgroup; thread 0 returns the total.
 __device__ __forceinline__ DriftAcc block_fold(DriftAcc a) {
     __shared__ DriftAcc s_acc[kThreads];
@@ -397,26 +421,6 @@ __device__ __forceinline__ DriftAcc block_fold(DriftAcc a) {
         __syncthreads();
     }
     return s_acc[0];
-}
-
-__global__ __launch_bounds__(kThreads) void k_drift_reduce(const DriftPartial* parts, int64_t count,
-                                                           DriftAcc* out) {
-    const int64_t per = (count + kReduceGroups - 1) / kReduceGroups;
-    const int64_t lo = (int64_t)blockIdx.x * per;
-    const int64_t hi = lo + per < count ? lo + per : count;
-    DriftAcc a;
-    a.zero();
-    int64_t j = lo + threadIdx.x;
-    for (; j + 3 * kThreads < hi; j += 4 * kThreads) {
-        DriftPartial q[4];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) q[u] = parts[j + u * kThreads];
-#pragma unroll
-        for (int u = 0; u < 4; ++u) a.add(q[u]);
-    }
-    for (; j < hi; j += kThreads) a.add(parts[j]);
-    const DriftAcc t = block_fold(a);
-    if (threadIdx.x == 0) out[blockIdx.x] = t;
 }
 
 // The ll_drift record from the folded totals (thread 0 of the caller).
@@ -435,14 +439,64 @@ __device__ __forceinline__ void write_drift(const DriftAcc& t, int n, int64_t d,
     *out = r;
 }
 
-__global__ __launch_bounds__(kThreads) void k_drift_final(const DriftAcc* groups, int n,
-                                                          int64_t d, int have_master,
-                                                          DriftOut* out) {
+// Device-coherent copies of a second-level partial (written by one
+// workgroup, read by another that may sit on another XCD).
+__device__ __forceinline__ void store_acc(DriftAcc* dst, const DriftAcc& a) {
+    __hip_atomic_store(&dst->pair, a.pair, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(&dst->abs_sum, a.abs_sum, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(&dst->range, a.range, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(&dst->stale, a.stale, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __hip_atomic_store(&dst->empty, a.empty, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ DriftAcc load_acc(const DriftAcc* src) {
+    DriftAcc a;
+    a.pair = __hip_atomic_load(&src->pair, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    a.abs_sum = __hip_atomic_load(&src->abs_sum, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    a.range = __hip_atomic_load(&src->range, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    a.stale = __hip_atomic_load(&src->stale, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    a.empty = __hip_atomic_load(&src->empty, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return a;
+}
+
+// Second level: kReduceGroups workgroups each fold a contiguous range of
+// partials; the last workgroup to finish (by a counter that the kernel which
+// wrote the partials zeroed) folds the kReduceGroups totals in a fixed order
+// and writes the record.  Every sum has a fixed order, so the result does not
+// depend on which workgroup finishes last.
+__global__ __launch_bounds__(kThreads) void k_drift_reduce(const DriftPartial* parts, int64_t count,
+                                                           DriftAcc* groups, int n, int64_t d,
+                                                           int have_master, DriftOut* out) {
+    __shared__ int s_last;
+    unsigned* counter = reduce_counter(groups);
+    const int64_t per = (count + kReduceGroups - 1) / kReduceGroups;
+    const int64_t lo = (int64_t)blockIdx.x * per;
+    const int64_t hi = lo + per < count ? lo + per : count;
     DriftAcc a;
     a.zero();
-    for (int j = threadIdx.x; j < kReduceGroups; j += kThreads) a.add(groups[j]);
+    int64_t j = lo + threadIdx.x;
+    for (; j + 3 * kThreads < hi; j += 4 * kThreads) {
+        DriftPartial q[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) q[u] = parts[j + u * kThreads];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) a.add(q[u]);
+    }
+    for (; j < hi; j += kThreads) a.add(parts[j]);
     const DriftAcc t = block_fold(a);
-    if (threadIdx.x == 0) write_drift(t, n, d, have_master, out);
+    if (threadIdx.x == 0) {
+        store_acc(groups + blockIdx.x, t);
+        __threadfence();
+        s_last = atomicAdd(counter, 1u) == gridDim.x - 1;
+    }
+    __syncthreads();
+    if (!s_last) return;
+    __threadfence();
+    DriftAcc b;
+    b.zero();
+    for (int g = threadIdx.x; g < kReduceGroups; g += kThreads) b.add(load_acc(groups + g));
+    const DriftAcc tot = block_fold(b);
+    if (threadIdx.x == 0) write_drift(tot, n, d, have_master, out);
 }
 
 // Few partials (small shards): one workgroup folds them directly, in a fixed
@@ -468,10 +522,7 @@ static hipError_t launch_drift_reduce(const DriftPartial* parts, int64_t count, 
         return hipGetLastError();
     }
     hipLaunchKernelGGL(k_drift_reduce, dim3(kReduceGroups), dim3(kThreads), 0, s, parts, count,
-                       groups);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(k_drift_final, dim3(1), dim3(kThreads), 0, s, groups, n, d, have_master, out);
+                       groups, n, d, have_master, out);
     return hipGetLastError();
 }
 
@@ -594,6 +645,7 @@ __device__ __forceinline__ void step_tile_w(const FusedParams& p, const Chunk& c
         const uint32_t stale = ch.c == 0 ? (uint32_t)(p.n - RC) : 0u;
         const uint32_t empty = (ch.c == 0 && K == 0) ? 1u : 0u;
         block_reduce_partial<NT>(pair, abs_sum, range, stale, empty, p.partials + tile);
+        if (tile == 0 && threadIdx.x == 0) *reduce_counter(p.groups) = 0u;
     }
 }
 
@@ -688,6 +740,17 @@ hipError_t launch_masks_bernoulli(int n, int64_t num_packets, uint64_t step, int
     const int64_t blocks = grid_cap((total + kThreads - 1) / kThreads);
     hipLaunchKernelGGL(k_masks_bernoulli, dim3((unsigned)blocks), dim3(kThreads), 0, s, n,
                        num_packets, step, (uint64_t)dir, seed, thr, owner, reliable, arrived);
+    return hipGetLastError();
+}
+
+hipError_t launch_masks_bernoulli_jobs(int n, int64_t num_packets, uint64_t step,
+                                       const MaskJob* jobs, int njobs, hipStream_t s) {
+    MaskJobs J;
+    for (int j = 0; j < njobs; ++j) J.job[j] = jobs[j];
+    const int64_t total = (int64_t)n * num_packets * njobs;
+    const int64_t blocks = grid_cap((total + kThreads - 1) / kThreads);
+    hipLaunchKernelGGL(k_masks_bernoulli_jobs, dim3((unsigned)blocks), dim3(kThreads), 0, s, n,
+                       num_packets, step, njobs, J);
     return hipGetLastError();
 }
 
@@ -931,16 +994,18 @@ static int64_t launch_fused_grd(const FusedParams& p, const PaceHint& h, hipStre
         // draws at the start of its round, all at once; where memory for
         // them is at hand they are drawn beforehand by the mask kernel and
         // the step reads them.
+        MaskJob jobs[2];
+        int njobs = 0;
         for (int dir = 0; dir < 2; ++dir) {
             if (!pp.src[dir].draw || !pp.pre[dir]) continue;
             const MaskSource& m = pp.src[dir];
-            hipError_t e = launch_masks_bernoulli(pp.n, pp.P, pp.step, dir, m.seed, m.thr, m.owner,
-                                                  m.reliable, pp.pre[dir], s);
-            if (e != hipSuccess) return -1;
+            jobs[njobs++] = MaskJob{(uint64_t)dir, m.seed, m.thr, m.owner, m.reliable, pp.pre[dir]};
             pp.src[dir] = MaskSource{false, 0, 0, pp.pre[dir], -1, nullptr};
             if (dir == 0 && pp.out_g == pp.pre[0]) pp.out_g = nullptr;
             if (dir == 1 && pp.out_b == pp.pre[1]) pp.out_b = nullptr;
         }
+        if (njobs && launch_masks_bernoulli_jobs(pp.n, pp.P, pp.step, jobs, njobs, s) != hipSuccess)
+            return -1;
         hipLaunchKernelGGL(k_pace_anchor, dim3(1), dim3(64), 0, s, margin);
         hipLaunchKernelGGL((k_step_paced<G, R, DRIFT>), dim3((unsigned)tiles), dim3(NT), 0, s, pp,
                            q);

@@ -55,7 +55,7 @@ def test_workspace_bytes_host_logic():
         return r256(n * S * 256) + r256(n * S) + r256(n)
     n, d, L = 64, 105_250_000, 4096
     P = (d + L - 1) // L
-    groups = 256 * 40  # second-level drift partials
+    groups = r256(256 * 40 + 16)  # second-level drift partials and their counter
     assert ll.ll_workspace_bytes(n, d, L) == (r256(P * 4 * 32) + groups + 2 * r256(n * P)
                                               + 2 * ge(n, P))
     assert ll.ll_workspace_bytes(4, 10, 8) == 256 + groups + 2 * 256 + 2 * ge(4, 2)
