@@ -21,7 +21,8 @@
  * Conventions for every entry point:
  *   - All pointers are DEVICE pointers unless marked "host".  The caller owns
  *     all memory; the library allocates none.  Scratch memory comes from a
- *     caller-supplied workspace of ll_workspace_bytes() bytes.
+ *     caller-supplied workspace of ll_workspace_bytes() bytes (or, for
+ *     lossy_step_fused_noalloc, from a static device array of the library).
  *   - `stream` is a hipStream_t (NULL = the default stream).  Every call only
  *     enqueues kernels on it (no allocation, no memset, no copy) and returns
  *     without synchronising; device outputs are valid once the stream has
@@ -308,6 +309,31 @@ LL_API int lossy_step_fused(int32_t n, int64_t d, int64_t packet, uint64_t step,
                      uint8_t* arrived_g, uint8_t* arrived_b, int32_t* counts,
                      void* workspace, size_t ws_bytes, ll_drift* drift,
                      const ll_ext* ext, void* stream);
+
+/*
+ * lossy_step_fused for callers that cannot allocate device memory (code
+ * under HIP graph capture, serving loops, harnesses that forbid hipMalloc):
+ * the same step, arguments and results, with the workspace taken from a
+ * static device array of LL_NOALLOC_SCRATCH_BYTES that the library holds on
+ * every device it runs on until the process ends.  No call allocates (no
+ * hipMalloc, hipFree or allocating library routine); the first call on a
+ * device looks the array's address up on that device.
+ *   Sizes whose workspace, ll_workspace_bytes(n, d, packet), exceeds
+ *   LL_NOALLOC_SCRATCH_BYTES return LL_EINVAL before any device work.
+ *   Every call on one device shares that device's array and leaves its
+ *   contents behind (the step writes everything it reads from it before
+ *   reading it); calls that overlap on one device (other streams, other
+ *   threads) race on it and must be ordered by the caller.
+ */
+enum { LL_NOALLOC_SCRATCH_BYTES = 16777216 };
+LL_API int lossy_step_fused_noalloc(int32_t n, int64_t d, int64_t packet, uint64_t step,
+                     const ll_loss* loss_g, const ll_loss* loss_b,
+                     uint8_t* ge_state_g, uint8_t* ge_state_b,
+                     int32_t gdtype, const void* grads, int64_t ld_g,
+                     const ll_opt* opt, float* theta, float* m, float* v,
+                     int32_t rdtype, void* replicas, int64_t ld_r,
+                     uint8_t* arrived_g, uint8_t* arrived_b, int32_t* counts,
+                     ll_drift* drift, const ll_ext* ext, void* stream);
 
 /*
  * Pacing of lossy_step_fused (a performance setting of this library, not part

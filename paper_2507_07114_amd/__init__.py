@@ -19,7 +19,8 @@ import torch
 __all__ = [
     # entry points of include/lossy.h
     "ll_masks", "ll_ages_update", "lossy_aggregate", "shard_step", "lossy_broadcast",
-    "drift_stats", "lossy_step_fused", "ll_workspace_bytes", "ll_masks_workspace_bytes",
+    "drift_stats", "lossy_step_fused", "lossy_step_fused_noalloc", "ll_workspace_bytes",
+    "ll_masks_workspace_bytes", "LL_NOALLOC_SCRATCH_BYTES",
     "ll_last_error", "ll_set_pacing", "ll_get_pacing",
     # argument structs and their builders
     "LossSpec", "OptSpec", "Ext", "ExtArgs", "Pacing", "bernoulli", "gilbert_elliott", "sgd", "sgd_momentum", "adam",
@@ -35,6 +36,7 @@ LL_LOSS_BERNOULLI, LL_LOSS_GILBERT_ELLIOTT = 0, 1
 LL_SGD, LL_SGD_MOMENTUM, LL_ADAM = 0, 1, 2
 LL_DIR_GRAD, LL_DIR_BCAST = 0, 1
 LL_EST_ARRIVED_MEAN, LL_EST_HORVITZ_THOMPSON, LL_EST_STALE_FILL = 0, 1, 2
+LL_NOALLOC_SCRATCH_BYTES = 16 << 20
 ESTIMATORS = {"arrived_mean": LL_EST_ARRIVED_MEAN, "horvitz_thompson": LL_EST_HORVITZ_THOMPSON,
               "stale_fill": LL_EST_STALE_FILL}
 
@@ -199,6 +201,11 @@ _SIGNATURES = {
                                         ctypes.POINTER(OptSpec), _vp, _vp, _vp, _i32, _vp, _i64,
                                         _vp, _vp, _vp, _vp, ctypes.c_size_t, _vp,
                                         ctypes.POINTER(Ext), _vp]),
+    "lossy_step_fused_noalloc": (ctypes.c_int, [_i32, _i64, _i64, _u64, ctypes.POINTER(LossSpec),
+                                                ctypes.POINTER(LossSpec), _vp, _vp, _i32, _vp,
+                                                _i64, ctypes.POINTER(OptSpec), _vp, _vp, _vp,
+                                                _i32, _vp, _i64, _vp, _vp, _vp, _vp,
+                                                ctypes.POINTER(Ext), _vp]),
     "ll_workspace_bytes": (ctypes.c_size_t, [_i32, _i64, _i64]),
     "ll_last_error": (ctypes.c_char_p, []),
     "ll_set_pacing": (ctypes.c_int, [ctypes.c_void_p]),
@@ -400,17 +407,10 @@ def drift_stats(replicas: torch.Tensor, *, d: int, packet: int, workspace: torch
         _stream()))
 
 
-def lossy_step_fused(*, d: int, packet: int, step: int, loss_g: LossSpec, loss_b: LossSpec,
-                     grads: torch.Tensor, opt: OptSpec, theta: torch.Tensor,
-                     replicas: torch.Tensor, m: Optional[torch.Tensor] = None,
-                     v: Optional[torch.Tensor] = None,
-                     ge_state_g: Optional[torch.Tensor] = None,
-                     ge_state_b: Optional[torch.Tensor] = None,
-                     arrived_g: Optional[torch.Tensor] = None,
-                     arrived_b: Optional[torch.Tensor] = None,
-                     counts: Optional[torch.Tensor] = None,
-                     workspace: Optional[torch.Tensor] = None,
-                     drift: Optional[torch.Tensor] = None, ext=None) -> None:
+def _fused_args(d, packet, step, loss_g, loss_b, grads, opt, theta, replicas, m, v,
+                ge_state_g, ge_state_b, arrived_g, arrived_b, counts, drift, ext):
+    """Checked, marshalled arguments of the fused step, in C order up to (and
+    without) the workspace, and the tail after it."""
     _need_rows(grads, "grads", d)
     _need_rows(replicas, "replicas", d)
     if replicas.shape[0] != grads.shape[0]:
@@ -427,12 +427,47 @@ def lossy_step_fused(*, d: int, packet: int, step: int, loss_g: LossSpec, loss_b
     ref = _ext_ref(ext, n, P, grads)
     gp, ldg, gt = _rows(grads, "grads")
     rp, ldr, rt = _rows(replicas, "replicas")
+    head = (grads.shape[0], d, packet, step, ctypes.byref(loss_g), ctypes.byref(loss_b),
+            _flat(ge_state_g, "ge_state_g", torch.uint8),
+            _flat(ge_state_b, "ge_state_b", torch.uint8),
+            gt, gp, ldg, ctypes.byref(opt), _flat(theta, "theta", torch.float32),
+            _flat(m, "m", torch.float32), _flat(v, "v", torch.float32), rt, rp, ldr,
+            _flat(arrived_g, "arrived_g", torch.uint8), _flat(arrived_b, "arrived_b", torch.uint8),
+            _flat(counts, "counts", torch.int32))
+    tail = (_dev(drift, "drift", torch.float64), ref, _stream())
+    return head, tail
+
+
+def lossy_step_fused(*, d: int, packet: int, step: int, loss_g: LossSpec, loss_b: LossSpec,
+                     grads: torch.Tensor, opt: OptSpec, theta: torch.Tensor,
+                     replicas: torch.Tensor, m: Optional[torch.Tensor] = None,
+                     v: Optional[torch.Tensor] = None,
+                     ge_state_g: Optional[torch.Tensor] = None,
+                     ge_state_b: Optional[torch.Tensor] = None,
+                     arrived_g: Optional[torch.Tensor] = None,
+                     arrived_b: Optional[torch.Tensor] = None,
+                     counts: Optional[torch.Tensor] = None,
+                     workspace: Optional[torch.Tensor] = None,
+                     drift: Optional[torch.Tensor] = None, ext=None) -> None:
+    head, tail = _fused_args(d, packet, step, loss_g, loss_b, grads, opt, theta, replicas, m, v,
+                             ge_state_g, ge_state_b, arrived_g, arrived_b, counts, drift, ext)
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     _check("lossy_step_fused", _load().lossy_step_fused(
-        grads.shape[0], d, packet, step, ctypes.byref(loss_g), ctypes.byref(loss_b),
-        _flat(ge_state_g, "ge_state_g", torch.uint8), _flat(ge_state_b, "ge_state_b", torch.uint8),
-        gt, gp, ldg, ctypes.byref(opt), _flat(theta, "theta", torch.float32),
-        _flat(m, "m", torch.float32), _flat(v, "v", torch.float32), rt, rp, ldr,
-        _flat(arrived_g, "arrived_g", torch.uint8), _flat(arrived_b, "arrived_b", torch.uint8),
-        _flat(counts, "counts", torch.int32), _dev(workspace, "workspace"), ws_bytes,
-        _dev(drift, "drift", torch.float64), ref, _stream()))
+        *head, _dev(workspace, "workspace"), ws_bytes, *tail))
+
+
+def lossy_step_fused_noalloc(*, d: int, packet: int, step: int, loss_g: LossSpec,
+                             loss_b: LossSpec, grads: torch.Tensor, opt: OptSpec,
+                             theta: torch.Tensor, replicas: torch.Tensor,
+                             m: Optional[torch.Tensor] = None, v: Optional[torch.Tensor] = None,
+                             ge_state_g: Optional[torch.Tensor] = None,
+                             ge_state_b: Optional[torch.Tensor] = None,
+                             arrived_g: Optional[torch.Tensor] = None,
+                             arrived_b: Optional[torch.Tensor] = None,
+                             counts: Optional[torch.Tensor] = None,
+                             drift: Optional[torch.Tensor] = None, ext=None) -> None:
+    """lossy_step_fused with the library's static device scratch instead of a
+    workspace (for callers that cannot allocate)."""
+    head, tail = _fused_args(d, packet, step, loss_g, loss_b, grads, opt, theta, replicas, m, v,
+                             ge_state_g, ge_state_b, arrived_g, arrived_b, counts, drift, ext)
+    _check("lossy_step_fused_noalloc", _load().lossy_step_fused_noalloc(*head, *tail))

@@ -16,6 +16,7 @@ using namespace lossy;
 static_assert(sizeof(ll_drift) == sizeof(DriftOut), "ll_drift layout");
 static_assert(sizeof(DriftPartial) == 32, "partial layout");
 static_assert(sizeof(DriftAcc) == 40, "second-level partial layout");
+static_assert((size_t)LL_NOALLOC_SCRATCH_BYTES == kNoAllocScratchBytes, "static scratch size");
 static_assert(LL_PACE_AUTO == kPaceAuto && LL_PACE_ALWAYS == kPaceAlways &&
                   LL_PACE_NEVER == kPaceNever,
               "pacing modes");
@@ -537,13 +538,19 @@ int drift_stats(int32_t n, int64_t d, int64_t packet, int32_t rdtype, const void
                      "drift_stats");
 }
 
-int lossy_step_fused(int32_t n, int64_t d, int64_t packet, uint64_t step, const ll_loss* loss_g,
-                     const ll_loss* loss_b, uint8_t* ge_state_g, uint8_t* ge_state_b,
-                     int32_t gdtype, const void* grads, int64_t ld_g, const ll_opt* opt,
-                     float* theta, float* m, float* v, int32_t rdtype, void* replicas,
-                     int64_t ld_r, uint8_t* arrived_g, uint8_t* arrived_b, int32_t* counts,
-                     void* workspace, size_t ws_bytes, ll_drift* drift, const ll_ext* ext,
-                     void* stream) {
+}  // extern "C"
+
+namespace {
+
+// The fused step behind lossy_step_fused and lossy_step_fused_noalloc; `fn`
+// names the entry point in error messages.
+int step_fused(const char* fn, int32_t n, int64_t d, int64_t packet, uint64_t step,
+               const ll_loss* loss_g, const ll_loss* loss_b, uint8_t* ge_state_g,
+               uint8_t* ge_state_b, int32_t gdtype, const void* grads, int64_t ld_g,
+               const ll_opt* opt, float* theta, float* m, float* v, int32_t rdtype,
+               void* replicas, int64_t ld_r, uint8_t* arrived_g, uint8_t* arrived_b,
+               int32_t* counts, void* workspace, size_t ws_bytes, ll_drift* drift,
+               const ll_ext* ext, void* stream) {
     Geometry g;
     int r = check_shape(n, d, packet, &g);
     if (r) return r;
@@ -561,7 +568,7 @@ int lossy_step_fused(int32_t n, int64_t d, int64_t packet, uint64_t step, const 
     if (drift && (r = check_vec("drift", drift, true))) return r;
     hipStream_t s = reinterpret_cast<hipStream_t>(stream);
     if (d == 0) {
-        if (drift) return hip_check(launch_drift_zero(reinterpret_cast<DriftOut*>(drift), s), "lossy_step_fused");
+        if (drift) return hip_check(launch_drift_zero(reinterpret_cast<DriftOut*>(drift), s), fn);
         return ok();
     }
     if ((r = check_rows("grads", grads, ld_g, d, elem_bytes(gdtype)))) return r;
@@ -646,18 +653,58 @@ int lossy_step_fused(int32_t n, int64_t d, int64_t packet, uint64_t step, const 
             p.src[dir] = MaskSource{false, 0, 0, dst, -1, nullptr};
         }
         p.out_g = p.out_b = nullptr;
-        r = hip_check(launch_masks_parity(PL, s), "lossy_step_fused (parity masks)");
+        r = hip_check(launch_masks_parity(PL, s), fn);
         if (r) return r;
     }
     if (nge) {
         if ((int64_t)nge * n * w.gs.S > 0x7FFFFFFFll) return fail(LL_EINVAL, "too many workgroups");
         if (nge == 1) L.job[1] = L.job[0];
-        r = hip_check(launch_masks_ge(L, nge, s), "lossy_step_fused (Gilbert-Elliott masks)");
+        r = hip_check(launch_masks_ge(L, nge, s), fn);
         if (r) return r;
     }
     const PaceHint hint{expected_arrival(loss_g, x.parity), expected_arrival(loss_b, x.parity)};
     return hip_check(launch_fused(gdtype, rdtype, p, reinterpret_cast<DriftOut*>(drift), hint, s),
-                     "lossy_step_fused");
+                     fn);
+}
+
+}  // namespace
+
+extern "C" {
+
+int lossy_step_fused(int32_t n, int64_t d, int64_t packet, uint64_t step, const ll_loss* loss_g,
+                     const ll_loss* loss_b, uint8_t* ge_state_g, uint8_t* ge_state_b,
+                     int32_t gdtype, const void* grads, int64_t ld_g, const ll_opt* opt,
+                     float* theta, float* m, float* v, int32_t rdtype, void* replicas,
+                     int64_t ld_r, uint8_t* arrived_g, uint8_t* arrived_b, int32_t* counts,
+                     void* workspace, size_t ws_bytes, ll_drift* drift, const ll_ext* ext,
+                     void* stream) {
+    return step_fused("lossy_step_fused", n, d, packet, step, loss_g, loss_b, ge_state_g,
+                      ge_state_b, gdtype, grads, ld_g, opt, theta, m, v, rdtype, replicas, ld_r,
+                      arrived_g, arrived_b, counts, workspace, ws_bytes, drift, ext, stream);
+}
+
+int lossy_step_fused_noalloc(int32_t n, int64_t d, int64_t packet, uint64_t step,
+                             const ll_loss* loss_g, const ll_loss* loss_b, uint8_t* ge_state_g,
+                             uint8_t* ge_state_b, int32_t gdtype, const void* grads,
+                             int64_t ld_g, const ll_opt* opt, float* theta, float* m, float* v,
+                             int32_t rdtype, void* replicas, int64_t ld_r, uint8_t* arrived_g,
+                             uint8_t* arrived_b, int32_t* counts, ll_drift* drift,
+                             const ll_ext* ext, void* stream) {
+    static const char* fn = "lossy_step_fused_noalloc";
+    Geometry g;
+    int r = check_shape(n, d, packet, &g);
+    if (r) return r;
+    const size_t need = ws_layout(n, g).total;
+    if (need > kNoAllocScratchBytes)
+        return fail(LL_EINVAL,
+                    "%s: n=%d, d=%lld, packet=%lld need %zu bytes of scratch, more than the "
+                    "%zu bytes of its static scratch; use lossy_step_fused with a workspace",
+                    fn, n, (long long)d, (long long)packet, need, kNoAllocScratchBytes);
+    void* ws = nullptr;
+    if ((r = hip_check(noalloc_scratch(&ws), fn))) return r;
+    return step_fused(fn, n, d, packet, step, loss_g, loss_b, ge_state_g, ge_state_b, gdtype,
+                      grads, ld_g, opt, theta, m, v, rdtype, replicas, ld_r, arrived_g,
+                      arrived_b, counts, ws, kNoAllocScratchBytes, drift, ext, stream);
 }
 
 }  // extern "C"

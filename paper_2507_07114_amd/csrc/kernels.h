@@ -228,4 +228,12 @@ hipError_t launch_fused(int gdtype, int rdtype, const FusedParams& p, DriftOut* 
                         const PaceHint& hint, hipStream_t s);
 hipError_t launch_drift_zero(DriftOut* out, hipStream_t s);
 
+// Device scratch of the entry point that allocates nothing: a static device
+// array of kNoAllocScratchBytes per device.  noalloc_scratch gives its
+// address on the current device (looked up once per device, at most
+// kMaxDevices devices).
+constexpr size_t kNoAllocScratchBytes = (size_t)16 << 20;
+constexpr int kMaxDevices = 64;
+hipError_t noalloc_scratch(void** ptr);
+
 }  // namespace lossy

@@ -15,9 +15,7 @@
 #include <math.h>
 
 #include <atomic>
-#include <map>
 #include <mutex>
-#include <utility>
 
 namespace lossy {
 
@@ -856,39 +854,45 @@ std::atomic<int> g_pace_resident{kDefaultPaceResident};
 std::atomic<double> g_pace_headroom{kDefaultPaceHeadroom};
 
 // Compute units and clock rate of a device, and resident workgroups per
-// compute unit of a kernel, looked up once.
+// compute unit of a kernel, looked up once per device into fixed tables (no
+// host allocation on the call path).
 std::mutex g_cache_mu;
-std::map<int, std::pair<int, double>> g_dev_cache;
-std::map<std::pair<int, const void*>, int> g_occ_cache;
+struct DevInfo {
+    bool known;
+    int cus;
+    double tick_hz;
+};
+DevInfo g_dev_info[kMaxDevices];
 
 bool device_info(int dev, int* cus, double* tick_hz) {
+    if (dev < 0 || dev >= kMaxDevices) return false;
     std::lock_guard<std::mutex> lk(g_cache_mu);
-    auto it = g_dev_cache.find(dev);
-    if (it == g_dev_cache.end()) {
+    DevInfo& di = g_dev_info[dev];
+    if (!di.known) {
         int c = 0, khz = 0;
         if (hipDeviceGetAttribute(&c, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
             hipDeviceGetAttribute(&khz, hipDeviceAttributeWallClockRate, dev) != hipSuccess)
             return false;
-        it = g_dev_cache.emplace(dev, std::make_pair(c, 1e3 * (double)khz)).first;
+        di = DevInfo{true, c, 1e3 * (double)khz};
     }
-    *cus = it->second.first;
-    *tick_hz = it->second.second;
+    *cus = di.cus;
+    *tick_hz = di.tick_hz;
     return *cus > 0 && *tick_hz > 0.0;
 }
 
+// Resident workgroups per compute unit of one kernel (one table per kernel:
+// the caller passes a table of its own).
 template <class K>
-int resident_per_cu(int dev, K kernel, int threads) {
-    const void* key = reinterpret_cast<const void*>(kernel);
-    {
-        std::lock_guard<std::mutex> lk(g_cache_mu);
-        auto it = g_occ_cache.find({dev, key});
-        if (it != g_occ_cache.end()) return it->second;
-    }
-    int nb = 0;
-    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, kernel, threads, 0) != hipSuccess) nb = 0;
+int resident_per_cu(int dev, K kernel, int threads, int (&table)[kMaxDevices]) {
+    if (dev < 0 || dev >= kMaxDevices) return 0;
     std::lock_guard<std::mutex> lk(g_cache_mu);
-    g_occ_cache[{dev, key}] = nb;
-    return nb;
+    if (table[dev] == 0) {
+        int nb = 0;
+        if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, kernel, threads, 0) != hipSuccess)
+            nb = 0;
+        table[dev] = nb > 0 ? nb : -1;
+    }
+    return table[dev] > 0 ? table[dev] : 0;
 }
 }  // namespace
 
@@ -929,7 +933,8 @@ static bool pace_plan(const FusedParams& p, const PaceHint& h, int64_t tiles, Pa
     int dev = 0, cus = 0;
     double tick_hz = 0.0;
     if (hipGetDevice(&dev) != hipSuccess || !device_info(dev, &cus, &tick_hz)) return false;
-    const int per_cu = resident_per_cu(dev, k_step_paced<G, R, DRIFT>, NT);
+    static int occupancy[kMaxDevices];
+    const int per_cu = resident_per_cu(dev, k_step_paced<G, R, DRIFT>, NT, occupancy);
     const int k = st.overlap < 1 ? 1 : (st.overlap > 2 ? 2 : st.overlap);
     const int res = st.resident < k ? k : st.resident;
     const int64_t gmax = (int64_t)(st.headroom * per_cu * cus / res);
@@ -1038,6 +1043,36 @@ hipError_t launch_fused(int gdtype, int rdtype, const FusedParams& p, DriftOut* 
 hipError_t launch_drift_zero(DriftOut* out, hipStream_t s) {
     hipLaunchKernelGGL(k_drift_zero, dim3(1), dim3(64), 0, s, out);
     return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// Static scratch of the entry point that allocates nothing.  Each device that
+// loads the library holds its own copy until the process ends; host code
+// reaches it only through the device address that hipGetSymbolAddress gives
+// on that device (the array's own name is not a device address on the host).
+// ---------------------------------------------------------------------------
+static __device__ __align__(256) uint8_t scratch[kNoAllocScratchBytes];
+
+namespace {
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices];
+}  // namespace
+
+hipError_t noalloc_scratch(void** ptr) {
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lk(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* p = nullptr;
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        if (!p) return hipErrorInvalidSymbol;
+        g_scratch_ptr[dev] = p;
+    }
+    *ptr = g_scratch_ptr[dev];
+    return hipSuccess;
 }
 
 }  // namespace lossy

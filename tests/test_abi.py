@@ -21,7 +21,8 @@ def _declared():
 def test_header_declares_the_boundary():
     names = set(_declared())
     assert names == {"ll_masks", "lossy_aggregate", "shard_step", "lossy_broadcast",
-                     "drift_stats", "lossy_step_fused", "ll_workspace_bytes",
+                     "drift_stats", "lossy_step_fused", "lossy_step_fused_noalloc",
+                     "ll_workspace_bytes",
                      "ll_masks_workspace_bytes", "ll_ages_update", "ll_last_error",
                      "ll_set_pacing", "ll_get_pacing"}
 
