@@ -149,7 +149,7 @@ def test_fused_parity_with_oracle(name):
         assert got["empty_packets"] == int((mg.sum(axis=0) == 0).sum())
         lens = ostep.packet_lengths(w.d, w.packet, packets)
         K_elem = np.repeat(orc["counts"], lens)
-        tol_th = parity.state_bounds(w.opt, t, orc, K_elem)["theta"]
+        tol_th = parity.state_bounds(parity.opt_as_given(w.opt), t, orc, so.prev, K_elem)["theta"]
         tol = np.where(np.repeat(mb, lens, axis=1).astype(bool),
                        (parity.BF16_REL * np.abs(x) if w.gdtype == wl.BF16 else 0) + tol_th, 0.0)
         dev_pair = 0.0

@@ -153,10 +153,9 @@ def test_random_configuration(cfg):
         assert np.array_equal(dev.counts.cpu().numpy(), mg.sum(axis=0)), f"step {t} counts"
         orc = ostep.lossy_step(d=w.d, packet=w.packet, packets=packets, gdtype=w.gdtype,
                                grads=g_host, theta=so.theta, m=so.m, v=so.v,
-                               replicas=so.replicas, arrived_g=mg, arrived_b=mb, opt=w.opt, t=t,
+                               replicas=so.replicas, arrived_g=mg, arrived_b=mb, opt=parity.opt_as_given(w.opt), t=t,
                                lam=cfg["lam"], estimator=est, q=q_of(t), g_prev=prev_o)
-        so.prev_replicas = so.replicas
-        so.theta, so.m, so.v, so.replicas = orc["theta"], orc["m"], orc["v"], orc["replicas"]
+        so.advance(orc)
         parity.compare_step(w, t, dev, so, orc, mb, f"case {cfg['case']} step {t}")
         # drift of the device's own replicas, recomputed by the oracle
         reps = parity.host_rows(dev.replicas, so.idx, w.gdtype)

@@ -137,8 +137,8 @@ def test_aggregate_never_reads_lost_rows():
 def test_shard_step_parity(kind):
     d = 100_003
     rng = np.random.default_rng(1)
-    opt = dict(kind=kind, lr=3e-4 if kind == "adam" else 0.01, momentum=0.9, beta1=0.9,
-               beta2=0.95, eps=1e-8)
+    opt = parity.opt_as_given(dict(kind=kind, lr=3e-4 if kind == "adam" else 0.01,
+                                   momentum=0.9, beta1=0.9, beta2=0.95, eps=1e-8))
     spec = {"sgd": ll.sgd(opt["lr"]), "momentum": ll.sgd_momentum(opt["lr"], 0.9),
             "adam": ll.adam(opt["lr"], 0.9, 0.95, 1e-8)}[kind]
     th = (rng.standard_normal(d) * 0.02).astype(np.float32)
@@ -157,16 +157,17 @@ def test_shard_step_parity(kind):
             th1, m1, v1 = ostep.sgd(th.astype(np.float64), G, opt["lr"]), None, None
         elif kind == "momentum":
             th1, m1 = ostep.sgd_momentum(th.astype(np.float64), m.astype(np.float64), G,
-                                         opt["lr"], 0.9)
+                                         opt["lr"], opt["momentum"])
             v1 = None
         else:
             th1, m1, v1 = ostep.adam(th.astype(np.float64), m.astype(np.float64),
-                                     v.astype(np.float64), G, t + 1, opt["lr"], 0.9, 0.95, 1e-8)
-        # identical inputs: 1e-5 of max(|x|, rms x), no propagated term
+                                     v.astype(np.float64), G, t + 1, opt["lr"], opt["beta1"],
+                                     opt["beta2"], opt["eps"])
+        # identical inputs: the update's own roundings, no propagated term
         orc = dict(g_hat=g, mean_abs=np.zeros(d), theta=th1.astype(np.float32),
                    m=None if m1 is None else m1.astype(np.float32),
                    v=None if v1 is None else v1.astype(np.float32))
-        b = parity.state_bounds(opt, t, orc)
+        b = parity.state_bounds(opt, t, orc, dict(theta=th, m=m, v=v))
         parity.check_close(d_th.cpu().numpy(), orc["theta"], b["theta"], "theta")
         if m1 is not None:
             parity.check_close(d_m.cpu().numpy(), orc["m"], b["m"], "m")

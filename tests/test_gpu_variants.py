@@ -220,10 +220,9 @@ def test_fused_variants_parity_with_oracle(est, owner, rel):
         assert np.array_equal(dev.arrived_b.cpu().numpy(), mb)
         orc = ostep.lossy_step(d=w.d, packet=w.packet, packets=packets, gdtype=w.gdtype,
                                grads=g_host, theta=so.theta, m=so.m, v=so.v,
-                               replicas=so.replicas, arrived_g=mg, arrived_b=mb, opt=w.opt, t=t,
+                               replicas=so.replicas, arrived_g=mg, arrived_b=mb, opt=parity.opt_as_given(w.opt), t=t,
                                estimator=est, q=q, g_prev=prev_o)
-        so.prev_replicas = so.replicas
-        so.theta, so.m, so.v, so.replicas = orc["theta"], orc["m"], orc["v"], orc["replicas"]
+        so.advance(orc)
         parity.compare_step(w, t, dev, so, orc, mb, f"{est} step {t}")
         ages_o = ostep.update_ages(ages_o, mb)
         assert np.array_equal(_ages_host(ages), ages_o), f"step {t}: ages"
@@ -313,10 +312,9 @@ def test_fused_parity_with_oracle(est, G, owner, rel):
         assert np.array_equal(dev.arrived_b.cpu().numpy(), mb)
         orc = ostep.lossy_step(d=w.d, packet=w.packet, packets=packets, gdtype=w.gdtype,
                                grads=g_host, theta=so.theta, m=so.m, v=so.v,
-                               replicas=so.replicas, arrived_g=mg, arrived_b=mb, opt=w.opt, t=t,
+                               replicas=so.replicas, arrived_g=mg, arrived_b=mb, opt=parity.opt_as_given(w.opt), t=t,
                                estimator=est, q=q, g_prev=prev_o)
-        so.prev_replicas = so.replicas
-        so.theta, so.m, so.v, so.replicas = orc["theta"], orc["m"], orc["v"], orc["replicas"]
+        so.advance(orc)
         parity.compare_step(w, t, dev, so, orc, mb, f"{est} parity step {t}")
         if est == "stale_fill":
             prev_o = orc["g_prev"]
@@ -374,10 +372,9 @@ def test_all_variants_at_once_with_oracle(est):
         assert np.array_equal(dev.arrived_b.cpu().numpy(), mb), f"step {t}"
         orc = ostep.lossy_step(d=w.d, packet=w.packet, packets=packets, gdtype=w.gdtype,
                                grads=g_host, theta=so.theta, m=so.m, v=so.v,
-                               replicas=so.replicas, arrived_g=mg, arrived_b=mb, opt=w.opt, t=t,
+                               replicas=so.replicas, arrived_g=mg, arrived_b=mb, opt=parity.opt_as_given(w.opt), t=t,
                                estimator=est, q=q, g_prev=prev_o)
-        so.prev_replicas = so.replicas
-        so.theta, so.m, so.v, so.replicas = orc["theta"], orc["m"], orc["v"], orc["replicas"]
+        so.advance(orc)
         parity.compare_step(w, t, dev, so, orc, mb, f"all variants {est} step {t}")
         ages_o = ostep.update_ages(ages_o, mb)
         assert np.array_equal(_ages_host(ages), ages_o), f"step {t}: ages"

@@ -1,7 +1,8 @@
 """The five workloads at full size, in the launch configuration the benchmark
 times (fused step with drift): masks and counts bit-exact over every packet,
-sampled packets compared with the oracle step by step, and the long-run
-drift of Theorem 3.1 on the 200-step N=64 workload."""
+sampled packets compared with the oracle step by step, the whole shard's
+drift figures against plain torch fp64 arithmetic, and the long-run drift of
+Theorem 3.1 on the 200-step N=64 workload."""
 import gc
 import math
 
@@ -55,6 +56,9 @@ def test_full_size_sampled_parity(name):
             assert r["stale_packets"] == int((mb == 0).sum())
             assert r["empty_packets"] == int((K == 0).sum())
             assert math.isfinite(r["mean_sq"]) and r["mean_sq"] >= 0
+            # the whole shard's drift figures, recomputed by plain torch fp64
+            parity.check_drift_close(r, parity.torch_drift(dev.replicas, dev.theta, w.d),
+                                     f"{name} step {t} drift")
             orc = so.step(t, g_host, mg, mb)
             parity.compare_step(w, t, dev, so, orc, mb[:, packets], f"{name} step {t}")
             so.upload(dev)
@@ -214,9 +218,9 @@ def test_full_size_variants_on_the_7b_shard():
         orc = ostep.lossy_step(d=w.d, packet=w.packet, packets=packets, gdtype=w.gdtype,
                                grads=g_host, theta=so.theta, m=so.m, v=so.v,
                                replicas=so.replicas, arrived_g=mg[:, packets],
-                               arrived_b=mb[:, packets], opt=w.opt, t=0,
+                               arrived_b=mb[:, packets], opt=parity.opt_as_given(w.opt), t=0,
                                estimator="horvitz_thompson", q=q[:, packets])
-        so.prev_replicas = so.replicas
+        so.advance(orc)
         parity.compare_step(w, 0, dev, so, orc, mb[:, packets], "7B shard, all variants")
     finally:
         del dev
