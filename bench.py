@@ -105,27 +105,67 @@ def read_pmc_traffic(expect_hash: str):
         return None
 
 
-def hbm_copy_probe(nbytes: int = 2 << 30, reps: int = 5) -> float:
-    """Device-to-device copy of a known size (torch's copy kernel): achievable
-    HBM bandwidth for a 50/50 read/write stream on this GPU, as context."""
+def _median_gbs(launch, reps: int = 3, batch: int = 5) -> float:
+    """Median rate of `launch()` (which enqueues one kernel on torch's current
+    stream and returns its bytes) over `reps` event-timed batches of `batch`
+    back-to-back calls, after one untimed call."""
     import numpy as np
     import torch
-    src = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda")
-    dst = torch.empty_like(src)
-    dst.copy_(src)
+    launch()
     torch.cuda.synchronize()
-    times = []
+    rates = []
     for _ in range(reps):
         a = torch.cuda.Event(enable_timing=True)
         b = torch.cuda.Event(enable_timing=True)
         a.record()
-        dst.copy_(src)
+        nbytes = sum(launch() for _ in range(batch))
         b.record()
         torch.cuda.synchronize()
-        times.append(a.elapsed_time(b))
+        rates.append(nbytes / (a.elapsed_time(b) * 1e-3) / 1e9)
+    return float(np.median(rates))
+
+
+def hbm_copy_probe(nbytes: int = 2 << 30, reps: int = 3) -> float:
+    """Device-to-device copy of a known size by the runtime (torch's copy
+    kernel), as context beside the hand-written probes."""
+    import torch
+    src = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+
+    def launch():
+        dst.copy_(src)
+        return 2 * nbytes
+    gbs = _median_gbs(launch, reps)
     del src, dst
     torch.cuda.empty_cache()
-    return 2 * nbytes / (float(np.median(times)) * 1e-3) / 1e9
+    return gbs
+
+
+def hbm_probes(rows_src=None, rows_dst=None, row_bytes: int = 0, nbytes: int = 2 << 30) -> dict:
+    """Achievable HBM rates (GB/s) from the hand-written probes of
+    libhbmprobe.so: a contiguous 16-byte copy, read-only and write-only
+    streams of 2 GiB, and, given the step's own row buffers, the step's
+    many-row shape (every row of the gradient buffer read, then every row of
+    the replica buffer written, 4 KiB of each row per workgroup)."""
+    import torch
+    from paper_2507_07114_amd import probe
+    sink = torch.zeros(probe.SINK_BYTES, dtype=torch.uint8, device="cuda")
+    a = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda")
+    b = torch.empty_like(a)
+    out = {
+        "copy_16B": _median_gbs(lambda: probe.hbm_probe_copy(a, b)),
+        "read_16B": _median_gbs(lambda: probe.hbm_probe_read(a, sink)),
+        "write_16B_nontemporal": _median_gbs(lambda: probe.hbm_probe_write(b)),
+    }
+    del a, b
+    torch.cuda.empty_cache()
+    if rows_src is not None and rows_dst is not None:
+        n = rows_src.shape[0]
+        out[f"rows_{n}r_{n}w"] = _median_gbs(
+            lambda: probe.hbm_probe_rows(rows_src, n, rows_dst, n, row_bytes, sink))
+        out[f"rows_{n}r"] = _median_gbs(
+            lambda: probe.hbm_probe_rows(rows_src, n, None, 0, row_bytes, sink))
+    return {k: round(v, 1) for k, v in out.items()}
 
 
 def cpu_model() -> str:
@@ -241,7 +281,7 @@ def main():
     name = args.workload or wl.METRIC_WORKLOAD
     w = wl.WORKLOADS[name]
     copy_gbs = hbm_copy_probe()
-    log(f"plain 2 GiB device copy: {copy_gbs:.0f} GB/s")
+    log(f"runtime 2 GiB device copy: {copy_gbs:.0f} GB/s")
     log(f"workload {name}: n={w.n} d={w.d} packet={w.packet} P={w.num_packets}")
     dev = DeviceState(w)
     ext = None
@@ -345,6 +385,12 @@ def main():
         wall = sum(ms) / 1e3
     drift = ll.read_drift(dev.drift)
 
+    # Bandwidth probes after the timed steps (the row probe overwrites the
+    # replicas): plain streams and the step's own row shape.
+    row_bytes = (w.d * w.elem_bytes) // 16 * 16
+    probes = hbm_probes(dev.grads, dev.replicas, row_bytes)
+    log(f"hbm probes (GB/s): {probes}")
+
     total_bytes = sum(b["total"] for b in per_step_bytes)
     ms_per_step = wall * 1e3 / args.steps
     value = total_bytes / wall / 1e9
@@ -387,6 +433,8 @@ def main():
         # loss-oblivious pass would move them (context for the count above)
         "dense_equivalent_bytes_per_step": 2 * w.n * w.d * w.elem_bytes + mean_b["state_rw"],
         "hbm_copy_probe_gbs": round(copy_gbs, 1),
+        "hbm_probes_gbs": probes,
+        "frac_of_best_copy_probe": round(value / probes["copy_16B"], 4),
         "roofline": {
             "bound": "hbm",
             "kernel": ("stage chain: masks x2, k_aggregate, k_shard_step, k_broadcast, k_drift "

@@ -1,7 +1,9 @@
-"""Build liblossy.so (the HIP library behind include/lossy.h) for gfx950.
+"""Build liblossy.so (the HIP library behind include/lossy.h) and
+libhbmprobe.so (the bandwidth probes behind include/hbm_probe.h) for gfx950.
 
 Usage: python -m paper_2507_07114_amd.build   (or build() from Python).
-The library is written next to this file so it travels with the source tree.
+The libraries are written next to this file so they travel with the source
+tree.
 """
 from __future__ import annotations
 
@@ -17,6 +19,7 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD_DIR = os.path.join(ROOT, "_build")
 LIB_PATH = os.path.join(PKG, "liblossy.so")
+PROBE_LIB_PATH = os.path.join(PKG, "libhbmprobe.so")
 
 ARCH = "gfx950"
 # -ffp-contract=off: every fused multiply-add in the kernels is explicit, so
@@ -29,6 +32,7 @@ COMMON = [
     f"-I{INCLUDE}", f"-I{CSRC}",
 ]
 SOURCES = ["kernels.hip", "api.cpp"]
+PROBE_SOURCES = ["probe.hip"]
 
 
 def _hipcc() -> str:
@@ -47,21 +51,33 @@ def _run(cmd):
     return out
 
 
-def build(verbose: bool = False) -> str:
-    """Compile every source for gfx950 and link liblossy.so; returns its path."""
-    hipcc = _hipcc()
-    os.makedirs(BUILD_DIR, exist_ok=True)
-    objs = []
-    cmds = []
-    for src in SOURCES:
+def _compile_jobs(hipcc, sources):
+    objs, cmds = [], []
+    for src in sources:
         obj = os.path.join(BUILD_DIR, os.path.splitext(src)[0] + ".o")
         objs.append(obj)
         cmds.append([hipcc, *COMMON, "-x", "hip", "-c", os.path.join(CSRC, src), "-o", obj])
-    with ThreadPoolExecutor(max_workers=len(cmds)) as ex:
-        outs = list(ex.map(_run, cmds))
-    tmp = LIB_PATH + ".tmp"
-    outs.append(_run([hipcc, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp]))
-    os.replace(tmp, LIB_PATH)
+    return objs, cmds
+
+
+def _link(hipcc, objs, path):
+    tmp = path + ".tmp"
+    out = _run([hipcc, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp])
+    os.replace(tmp, path)
+    return out
+
+
+def build(verbose: bool = False) -> str:
+    """Compile every source for gfx950 and link liblossy.so and
+    libhbmprobe.so; returns the path of liblossy.so."""
+    hipcc = _hipcc()
+    os.makedirs(BUILD_DIR, exist_ok=True)
+    objs, cmds = _compile_jobs(hipcc, SOURCES)
+    pobjs, pcmds = _compile_jobs(hipcc, PROBE_SOURCES)
+    with ThreadPoolExecutor(max_workers=len(cmds) + len(pcmds)) as ex:
+        outs = list(ex.map(_run, cmds + pcmds))
+    outs.append(_link(hipcc, objs, LIB_PATH))
+    outs.append(_link(hipcc, pobjs, PROBE_LIB_PATH))
     if verbose:
         for o in outs:
             if o.strip():

@@ -262,3 +262,28 @@ def test_pacing_setting_round_trips_and_rejects_bad_values():
         assert ll.ll_get_pacing() == want
     finally:
         ll.ll_set_pacing(**before)
+
+
+PROBE_HEADER = os.path.join(ROOT, "include", "hbm_probe.h")
+
+
+def test_probe_library_exports_its_header_and_rejects_bad_arguments():
+    from paper_2507_07114_amd import probe
+    names = re.findall(r"^HBM_PROBE_API\s+[\w\s\*]*?\b(\w+)\s*\(", open(PROBE_HEADER).read(),
+                       flags=re.M)
+    assert set(names) == {"hbm_probe_copy", "hbm_probe_read", "hbm_probe_write",
+                          "hbm_probe_rows"}
+    lib = probe._load()
+    for name in names:
+        assert hasattr(lib, name), name
+        assert callable(getattr(probe, name)), name
+    # host-side checks only: none of these reaches a launch
+    assert lib.hbm_probe_copy(16, 32, 15, None) == -1          # size not a multiple of 16
+    assert lib.hbm_probe_copy(8, 32, 16, None) == -1           # misaligned source
+    assert lib.hbm_probe_copy(None, 32, 16, None) == -1
+    assert lib.hbm_probe_read(16, 16, None, None) == -1        # no sink
+    assert lib.hbm_probe_write(24, 16, None) == -1
+    assert lib.hbm_probe_rows(16, 0, 32, 0, 16, 16, 64, None) == -1    # nothing to move
+    assert lib.hbm_probe_rows(16, 2, 32, 2, 32, 16, 64, None) == -1    # ld < row
+    assert lib.hbm_probe_rows(16, 2, None, 1, 32, 32, 64, None) == -1  # missing dst
+    assert lib.hbm_probe_copy(16, 32, 0, None) == 0                    # nothing to copy
