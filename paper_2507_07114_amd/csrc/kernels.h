@@ -153,12 +153,14 @@ struct PaceParams {
     uint64_t late;                 // lateness past which a workgroup keeps its own pace, ticks
 };
 
-// Pacing modes and defaults: auto paces steps of at least kPaceMinRounds
+// Pacing modes and defaults: auto paces steps of bf16 rows, at least
+// kPaceMinRows of them, spanning at least kPaceMinRounds
 // rounds; the schedule is laid out for kDefaultPaceRate bytes/s with
 // kDefaultPaceGapUs between the gradient and replica sweeps, and starts
 // kPaceMarginUs after the anchor is written.
 enum { kPaceAuto = 0, kPaceAlways = 1, kPaceNever = 2 };
 constexpr int64_t kPaceMinRounds = 8;
+constexpr int kPaceMinRows = 32;
 constexpr double kDefaultPaceRate = 6.25e12;
 constexpr double kDefaultPaceGapUs = 2.0;
 constexpr double kDefaultPaceLeadUs = 4.0;
