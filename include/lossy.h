@@ -374,7 +374,7 @@ LL_API int lossy_step_fused_noalloc(int32_t n, int64_t d, int64_t packet, uint64
  *                them, and rounds start no closer than a round's length /
  *                resident apart, so that every round's workgroups find places
  *                when it starts.
- *   headroom     fraction of those places the rounds fill ((0, 1]; 0.9).
+ *   headroom     fraction of those places the rounds fill ((0, 1]; 1.0).
  * A workgroup that starts more than 10 us behind its round (its place freed
  * late) keeps the round's pace from its own start rather than rushing
  * through the slots it missed; smaller lateness is caught up.

@@ -171,7 +171,7 @@ constexpr double kPaceTailUs = 2.5;
 // Lateness past which a workgroup keeps its round's pace from its own start.
 constexpr double kPaceLateUs = 10.0;
 // Fraction of the resident workgroup places the rounds in flight may fill.
-constexpr double kDefaultPaceHeadroom = 0.9;
+constexpr double kDefaultPaceHeadroom = 1.0;
 
 // How the fused step is paced (process-wide; see ll_set_pacing).
 struct PaceSetting {
