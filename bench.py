@@ -32,7 +32,7 @@ sys.path.insert(0, HERE)
 
 HBM_PEAK_GBS = 8000.0
 METRIC = "aggregate+step+broadcast GB/s and % of HBM peak; N=64 7B-shard step"
-PMC_PROFILE = os.path.join(HERE, "profiles", "k_step_fused_n64_llama7b_shard_pmc.txt")
+PMC_PROFILE = os.path.join(HERE, "profiles", "k_step_paced_n64_llama7b_shard_pmc.txt")
 KERNEL_SOURCES = ["paper_2507_07114_amd/csrc/kernels.hip",
                   "paper_2507_07114_amd/csrc/lossy_device.h",
                   "paper_2507_07114_amd/csrc/kernels.h"]
@@ -439,7 +439,8 @@ def main():
             "bound": "hbm",
             "kernel": ("stage chain: masks x2, k_aggregate, k_shard_step, k_broadcast, k_drift "
                        "(+ reductions)") if args.stagewise else
-                      "k_step_fused (+ k_drift_reduce, k_drift_final)",
+                      "lossy_step_fused: k_step_paced or k_step_fused (+ mask, anchor and "
+                      "drift-fold launches)",
             "achieved": round(achieved, 2),
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
