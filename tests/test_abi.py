@@ -287,3 +287,65 @@ def test_probe_library_exports_its_header_and_rejects_bad_arguments():
     assert lib.hbm_probe_rows(16, 2, 32, 2, 32, 16, 64, None) == -1    # ld < row
     assert lib.hbm_probe_rows(16, 2, None, 1, 32, 32, 64, None) == -1  # missing dst
     assert lib.hbm_probe_copy(16, 32, 0, None) == 0                    # nothing to copy
+
+
+def test_binding_checks_every_buffer_against_the_sizes():
+    # Each mismatch between a buffer and (n, d, P) is refused by the binding
+    # before any device pointer is taken (CPU tensors suffice to show it).
+    import pytest
+    import torch
+    n, d, L = 4, 40, 8
+    P = 5
+    bf, f32, u8 = torch.bfloat16, torch.float32, torch.uint8
+
+    def args(**over):
+        a = dict(d=d, packet=L, step=0, loss_g=ll.bernoulli(0.1), loss_b=ll.bernoulli(0.1),
+                 grads=torch.zeros((n, 48), dtype=bf), opt=ll.adam(3e-4, 0.9, 0.95, 1e-8),
+                 theta=torch.zeros(d), replicas=torch.zeros((n, 48), dtype=bf),
+                 m=torch.zeros(d), v=torch.zeros(d), arrived_g=torch.zeros((n, P), dtype=u8),
+                 arrived_b=torch.zeros((n, P), dtype=u8),
+                 counts=torch.zeros(P, dtype=torch.int32), drift=torch.zeros(6, dtype=torch.float64))
+        a.update(over)
+        return a
+
+    cases = [
+        (dict(theta=torch.zeros(d - 1)), "theta has 39 elements"),
+        (dict(m=torch.zeros(d - 8)), "m has 32 elements"),
+        (dict(v=torch.zeros(d, dtype=torch.float64)), "v must have dtype"),
+        (dict(arrived_g=torch.zeros((n, P - 1), dtype=u8)), "arrived_g must have shape"),
+        (dict(arrived_b=torch.zeros((n + 1, P), dtype=u8)), "arrived_b must have shape"),
+        (dict(arrived_g=torch.zeros((n, P), dtype=torch.int8)), "arrived_g must have dtype"),
+        (dict(counts=torch.zeros(P - 1, dtype=torch.int32)), "counts has 4 elements"),
+        (dict(drift=torch.zeros(5, dtype=torch.float64)), "drift has 5 elements"),
+        (dict(replicas=torch.zeros((n - 1, 48), dtype=bf)), "same number of rows"),
+        (dict(grads=torch.zeros((n, d - 1), dtype=bf)), "fewer than d"),
+        (dict(ge_state_g=torch.zeros(n - 1, dtype=u8)), "ge_state_g has 3 elements"),
+        (dict(ext=ll.ext(ages=torch.zeros((n, P + 1), dtype=torch.int16))), "ages must have shape"),
+        (dict(ext=ll.ext(reliable=torch.zeros(P - 1, dtype=u8))), "reliable has 4 elements"),
+        # g_prev must match grads in shape, row stride and dtype
+        (dict(ext=ll.ext(estimator="stale_fill", g_prev=torch.zeros((n, d), dtype=bf))),
+         "g_prev must match grads"),
+        (dict(ext=ll.ext(estimator="stale_fill", g_prev=torch.zeros((n, 48), dtype=f32))),
+         "g_prev must match grads"),
+        (dict(ext=ll.ext(estimator="stale_fill",
+                         g_prev=torch.zeros((n, 64), dtype=bf)[:, :48])), "g_prev must match grads"),
+    ]
+    for over, msg in cases:
+        with pytest.raises(ValueError, match=msg):
+            ll.lossy_step_fused(**args(**over))
+    # the aggregate and the other stages check their own buffers too
+    with pytest.raises(ValueError, match="g_hat has 39 elements"):
+        ll.lossy_aggregate(torch.zeros((n, 48), dtype=bf), torch.zeros((n, P), dtype=u8), d=d,
+                           packet=L, g_hat=torch.zeros(d - 1))
+    with pytest.raises(ValueError, match="counts has 4 elements"):
+        ll.lossy_aggregate(torch.zeros((n, 48), dtype=bf), torch.zeros((n, P), dtype=u8), d=d,
+                           packet=L, g_hat=torch.zeros(d), counts=torch.zeros(P - 1, dtype=torch.int32))
+    with pytest.raises(ValueError, match="g_prev must match grads"):
+        ll.lossy_aggregate(torch.zeros((n, 48), dtype=bf), torch.zeros((n, P), dtype=u8), d=d,
+                           packet=L, g_hat=torch.zeros(d),
+                           ext=ll.ext(estimator="stale_fill", g_prev=torch.zeros((n, 40), dtype=bf)))
+    with pytest.raises(ValueError, match="arrived_bc must have shape"):
+        ll.lossy_broadcast(torch.zeros(d), torch.zeros((n, 48), dtype=bf),
+                           torch.zeros((n, P + 1), dtype=u8), d=d, packet=L)
+    with pytest.raises(ValueError, match="ages must have shape"):
+        ll.ll_ages_update(torch.zeros((n, P), dtype=u8), torch.zeros((n, P - 1), dtype=torch.int16))
