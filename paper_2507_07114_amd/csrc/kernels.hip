@@ -410,15 +410,25 @@ __global__ __launch_bounds__(R::kPacketThreads) void k_drift(DriftParams p) {
 // Fixed-order reduction of the per-workgroup partials into the ll_drift
 // record.
 // Fixed-order tree over the workgroup; thread 0 returns the total.
+template <int NT>
 __device__ __forceinline__ DriftAcc block_fold(DriftAcc a) {
-    __shared__ DriftAcc s_acc[kThreads];
+    __shared__ DriftAcc s_acc[NT];
     s_acc[threadIdx.x] = a;
     __syncthreads();
-    for (int off = kThreads / 2; off > 0; off >>= 1) {
+    for (int off = NT / 2; off > 0; off >>= 1) {
         if ((int)threadIdx.x < off) s_acc[threadIdx.x].add(s_acc[threadIdx.x + off]);
         __syncthreads();
     }
     return s_acc[0];
+}
+
+// Counts one finished workgroup once this thread's earlier stores have
+// completed.  The group totals are written with device-coherent stores and
+// read with device-coherent loads, so waiting for the stores is all the
+// ordering needed (a device-scope fence would also write back the L2).
+__device__ __forceinline__ unsigned count_done(unsigned* counter) {
+    __builtin_amdgcn_s_waitcnt(0);
+    return __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // The ll_drift record from the folded totals (thread 0 of the caller).
@@ -481,43 +491,43 @@ __global__ __launch_bounds__(kThreads) void k_drift_reduce(const DriftPartial* p
         for (int u = 0; u < 4; ++u) a.add(q[u]);
     }
     for (; j < hi; j += kThreads) a.add(parts[j]);
-    const DriftAcc t = block_fold(a);
+    const DriftAcc t = block_fold<kThreads>(a);
     if (threadIdx.x == 0) {
         store_acc(groups + blockIdx.x, t);
-        __threadfence();
-        s_last = atomicAdd(counter, 1u) == gridDim.x - 1;
+        s_last = count_done(counter) == gridDim.x - 1;
     }
     __syncthreads();
     if (!s_last) return;
-    __threadfence();
     DriftAcc b;
     b.zero();
     for (int g = threadIdx.x; g < kReduceGroups; g += kThreads) b.add(load_acc(groups + g));
-    const DriftAcc tot = block_fold(b);
+    const DriftAcc tot = block_fold<kThreads>(b);
     if (threadIdx.x == 0) write_drift(tot, n, d, have_master, out);
 }
 
-// Up to kDirectFold partials: one workgroup folds them directly, in a fixed
-// order (N = 8 step, 8192 partials: 8.1 us against 10.2 us for two levels).
+// Up to kDirectFold partials: one workgroup of kFoldThreads folds them
+// directly, in a fixed order, each thread with eight loads in flight (N = 8
+// step, 8192 partials: 8.2 us, against 10.2 us for two levels; 1024 threads
+// took as long).
+constexpr int kFoldThreads = 256;
 constexpr int64_t kDirectFold = 16384;
 
-__global__ __launch_bounds__(kThreads) void k_drift_direct(const DriftPartial* parts, int64_t count,
-                                                           int n, int64_t d, int have_master,
-                                                           DriftOut* out) {
+__global__ __launch_bounds__(kFoldThreads) void k_drift_direct(const DriftPartial* parts,
+                                                               int64_t count, int n, int64_t d,
+                                                               int have_master, DriftOut* out) {
     DriftAcc a;
     a.zero();
-    // each thread folds its partials j = t, t + kThreads, ... in order, eight
-    // loads in flight
+    // thread t folds partials j = t, t + kFoldThreads, ... in order
     int64_t j = threadIdx.x;
-    for (; j + 7 * kThreads < count; j += 8 * kThreads) {
+    for (; j + 7 * kFoldThreads < count; j += 8 * kFoldThreads) {
         DriftPartial q[8];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) q[u] = parts[j + u * kThreads];
+        for (int u = 0; u < 8; ++u) q[u] = parts[j + u * kFoldThreads];
 #pragma unroll
         for (int u = 0; u < 8; ++u) a.add(q[u]);
     }
-    for (; j < count; j += kThreads) a.add(parts[j]);
-    const DriftAcc t = block_fold(a);
+    for (; j < count; j += kFoldThreads) a.add(parts[j]);
+    const DriftAcc t = block_fold<kFoldThreads>(a);
     if (threadIdx.x == 0) write_drift(t, n, d, have_master, out);
 }
 
@@ -525,7 +535,7 @@ static hipError_t launch_drift_reduce(const DriftPartial* parts, int64_t count, 
                                       int n, int64_t d, int have_master, DriftOut* out,
                                       hipStream_t s) {
     if (count <= kDirectFold) {
-        hipLaunchKernelGGL(k_drift_direct, dim3(1), dim3(kThreads), 0, s, parts, count, n, d,
+        hipLaunchKernelGGL(k_drift_direct, dim3(1), dim3(kFoldThreads), 0, s, parts, count, n, d,
                            have_master, out);
         return hipGetLastError();
     }
