@@ -375,6 +375,8 @@ LL_API int lossy_step_fused_noalloc(int32_t n, int64_t d, int64_t packet, uint64
  *                resident apart, so that every round's workgroups find places
  *                when it starts.
  *   headroom     fraction of those places the rounds fill ((0, 1]; 1.0).
+ *   tail_us      time after a round's last slot before the next round may
+ *                count on its places ([0, 1e4]; default 2.5).
  * A workgroup that starts more than 10 us behind its round (its place freed
  * late) keeps the round's pace from its own start rather than rushing
  * through the slots it missed; smaller lateness is caught up.
@@ -387,7 +389,8 @@ LL_API int lossy_step_fused_noalloc(int32_t n, int64_t d, int64_t packet, uint64
  * device variable.  Overlapping paced steps on one device can read each
  * other's start time, which costs speed but changes no result.
  * ll_set_pacing returns LL_EINVAL for an unknown mode or a field outside the
- * ranges above (bytes_per_s in (0, 1e15), gap_us and lead_us in [0, 1e4]);
+ * ranges above (bytes_per_s in (0, 1e15), gap_us, lead_us and tail_us in
+ * [0, 1e4]);
  * ll_get_pacing fills `out` (host).
  */
 enum { LL_PACE_AUTO = 0, LL_PACE_ALWAYS = 1, LL_PACE_NEVER = 2 };
@@ -399,6 +402,7 @@ typedef struct {
     int32_t overlap;
     int32_t resident;
     double headroom;
+    double tail_us;
 } ll_pacing;
 
 LL_API int ll_set_pacing(const ll_pacing* cfg);

@@ -344,8 +344,10 @@ int ll_set_pacing(const ll_pacing* cfg) {
         return fail(LL_EINVAL, "resident=%d must lie in [overlap, 4]", cfg->resident);
     if (!(cfg->headroom > 0.0 && cfg->headroom <= 1.0))
         return fail(LL_EINVAL, "headroom must lie in (0, 1]");
+    if (!(cfg->tail_us >= 0.0 && cfg->tail_us <= 1e4))
+        return fail(LL_EINVAL, "tail_us must lie in [0, 1e4]");
     set_pace_setting(PaceSetting{cfg->mode, cfg->bytes_per_s, cfg->gap_us, cfg->lead_us,
-                                 cfg->overlap, cfg->resident, cfg->headroom});
+                                 cfg->overlap, cfg->resident, cfg->headroom, cfg->tail_us});
     return ok();
 }
 
@@ -359,6 +361,7 @@ int ll_get_pacing(ll_pacing* out) {
     out->overlap = st.overlap;
     out->resident = st.resident;
     out->headroom = st.headroom;
+    out->tail_us = st.tail_us;
     return ok();
 }
 

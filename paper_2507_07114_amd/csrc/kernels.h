@@ -167,7 +167,7 @@ constexpr double kDefaultPaceLeadUs = 4.0;
 constexpr int kDefaultPaceOverlap = 1;
 constexpr int kDefaultPaceResident = 1;
 constexpr double kPaceMarginUs = 3.0;
-constexpr double kPaceTailUs = 2.5;
+constexpr double kDefaultPaceTailUs = 2.5;
 // Lateness past which a workgroup keeps its round's pace from its own start.
 constexpr double kPaceLateUs = 10.0;
 // Fraction of the resident workgroup places the rounds in flight may fill.
@@ -182,6 +182,7 @@ struct PaceSetting {
     int overlap;         // rounds streaming at once (1 or 2)
     int resident;        // rounds the resident workgroup places are shared by (>= overlap)
     double headroom;     // fraction of the resident places the rounds may fill
+    double tail_us;      // allowance after a round's last slot
 };
 PaceSetting get_pace_setting();
 void set_pace_setting(const PaceSetting& s);

@@ -223,36 +223,6 @@ __global__ __launch_bounds__(kThreads) void k_ge_apply(GeLaunch L) {
     if (b.s == L.S - 1 && threadIdx.x == kThreads - 1) J.state[b.i] = (uint8_t)x;
 }
 
-// ---------------------------------------------------------------------------
-// Per-packet chunk geometry
-// ---------------------------------------------------------------------------
-struct Chunk {
-    int64_t k;    // packet
-    int c;        // chunk within the packet
-    int64_t e0;   // first element of this thread
-    int nv;       // valid elements of this thread (0..8)
-    bool whole;   // wave-uniform: every thread owns 0 or 8 elements, 16-byte aligned
-};
-
-// Chunk of tile b (tile = packet * cpp + chunk within the packet).  A chunk
-// is whole when it starts on a multiple of 8 elements and its valid part
-// ends on one or fills it: then every access of the tile can be a 16-byte
-// vector (row starts are 16-byte aligned).
-template <int NT>
-__device__ __forceinline__ Chunk chunk_at(int64_t b, int64_t d, int64_t L, int cpp) {
-    Chunk ch;
-    ch.k = b / cpp;
-    ch.c = (int)(b - ch.k * cpp);
-    const int64_t pk0 = ch.k * L;
-    const int64_t pend = pk0 + L < d ? pk0 + L : d;
-    const int64_t c0 = pk0 + (int64_t)ch.c * (NT * kElems);
-    ch.e0 = c0 + (int64_t)threadIdx.x * kElems;
-    const int64_t rem = pend - ch.e0;
-    ch.nv = rem <= 0 ? 0 : (rem >= 8 ? 8 : (int)rem);
-    ch.whole = (c0 % 8 == 0) && ((pend - c0) % 8 == 0 || pend >= c0 + NT * kElems);
-    return ch;
-}
-
 template <int NT>
 __device__ __forceinline__ Chunk chunk_of(int64_t d, int64_t L, int cpp) {
     return chunk_at<NT>(blockIdx.x, d, L, cpp);
@@ -263,14 +233,14 @@ __device__ __forceinline__ Chunk chunk_of(int64_t d, int64_t L, int cpp) {
 // ---------------------------------------------------------------------------
 template <class G, bool W>
 __device__ __forceinline__ void aggregate_chunk(const AggParams& p, const Chunk& ch,
-                                                const uint64_t* words, int nw, int K) {
+                                                const uint64_t* words, int K) {
     float th[8] = {0, 0, 0, 0, 0, 0, 0, 0};
     if (K == 0 && p.lam != 0.0f && p.var.kind == kEstArrivedMean)
         load8<F32, W>(p.theta + ch.e0, ch.nv, th);
     const bool relp = p.var.reliable != nullptr && p.var.reliable[ch.k] != 0;
     float g[8];
-    aggregate8<G, W>(reinterpret_cast<const typename G::T*>(p.grads), p.ld, ch.e0, ch.nv, words,
-                     nw, p.n, K, p.lam, th, p.var, relp, NoPace(), g);
+    aggregate8<G, W>(reinterpret_cast<const typename G::T*>(p.grads), p.ld, ch, words, p.n, K,
+                     p.lam, th, p.var, relp, NoPace(), g);
     store_f32x8<W>(p.g_hat + ch.e0, ch.nv, g);
 }
 
@@ -279,15 +249,15 @@ __global__ __launch_bounds__(G::kPacketThreads) void k_aggregate(AggParams p) {
     constexpr int NT = G::kPacketThreads;
     __shared__ uint64_t s_words[1][kMaxWords];
     const Chunk ch = chunk_of<NT>(p.d, p.L, p.cpp);
-    MaskSource src{false, 0, 0, p.arrived, -1, nullptr};
+    const MaskSource src[1] = {{false, 0, 0, p.arrived, -1, nullptr}};
     const int dirs[1] = {0};
-    stage_masks<NT>(1, &src, p.n, p.P, ch.k, 0, dirs, s_words);
+    stage_masks<NT, 1>(src, p.n, p.P, ch.k, 0, dirs, s_words);
     const int nw = (p.n + 63) >> 6;
     const int K = popcount_words(s_words[0], nw);
     if (ch.c == 0 && threadIdx.x == 0 && p.counts) p.counts[ch.k] = K;
     if (ch.nv == 0) return;
-    if (ch.whole) aggregate_chunk<G, true>(p, ch, s_words[0], nw, K);
-    else aggregate_chunk<G, false>(p, ch, s_words[0], nw, K);
+    if (ch.whole) aggregate_chunk<G, true>(p, ch, s_words[0], K);
+    else aggregate_chunk<G, false>(p, ch, s_words[0], K);
 }
 
 template <bool W>
@@ -338,9 +308,9 @@ __global__ __launch_bounds__(R::kPacketThreads) void k_broadcast(BcastParams p) 
     constexpr int NT = R::kPacketThreads;
     __shared__ uint64_t s_words[1][kMaxWords];
     const Chunk ch = chunk_of<NT>(p.d, p.L, p.cpp);
-    MaskSource src{false, 0, 0, p.arrived, -1, nullptr};
+    const MaskSource src[1] = {{false, 0, 0, p.arrived, -1, nullptr}};
     const int dirs[1] = {1};
-    stage_masks<NT>(1, &src, p.n, p.P, ch.k, 0, dirs, s_words);
+    stage_masks<NT, 1>(src, p.n, p.P, ch.k, 0, dirs, s_words);
     if (ch.nv == 0) return;
     const int nw = (p.n + 63) >> 6;
     if (ch.whole) broadcast_chunk<R, true>(p, ch, s_words[0], nw);
@@ -393,9 +363,9 @@ __global__ __launch_bounds__(R::kPacketThreads) void k_drift(DriftParams p) {
     const int nw = (p.n + 63) >> 6;
     uint32_t stale = 0;
     if (p.arrived) {
-        MaskSource src{false, 0, 0, p.arrived, -1, nullptr};
+        const MaskSource src[1] = {{false, 0, 0, p.arrived, -1, nullptr}};
         const int dirs[1] = {1};
-        stage_masks<NT>(1, &src, p.n, p.P, ch.k, 0, dirs, s_words);
+        stage_masks<NT, 1>(src, p.n, p.P, ch.k, 0, dirs, s_words);
         if (ch.c == 0) stale = (uint32_t)(p.n - popcount_words(s_words[0], nw));
     }
     double pair = 0.0, range = 0.0, abs_sum = 0.0;
@@ -564,8 +534,8 @@ __device__ __forceinline__ void step_chunk(const FusedParams& p, const Chunk& ch
     if (var.ge_derived && !relp) var.invq = ge_invq(var, p.step, ch.k, p.P);
     float th[8], mm[8], vv[8], g[8];
     unpack(th_r, th);
-    aggregate8<G, W>(reinterpret_cast<const typename G::T*>(p.grads), p.ld_g, ch.e0, ch.nv,
-                     s_words[0], nw, p.n, K, p.lam, th, var, relp, pace, g);
+    aggregate8<G, W>(reinterpret_cast<const typename G::T*>(p.grads), p.ld_g, ch, s_words[0], p.n,
+                     K, p.lam, th, var, relp, pace, g);
     if (p.opt.kind >= 1) unpack(m_r, mm);
     if (p.opt.kind == 2) unpack(v_r, vv);
     update8(p.opt, th, mm, vv, g);
@@ -594,33 +564,14 @@ __device__ __forceinline__ void step_chunk(const FusedParams& p, const Chunk& ch
 #pragma unroll
     for (int j = 0; j < 8; ++j) rv[j] = r.value(j);
     acc.init(RC > 0, rv);
-    for (int w = 0; w < nw; ++w) {
-        const uint64_t valid = (w == nw - 1 && last_bits < 64) ? ((1ull << last_bits) - 1) : ~0ull;
-        uint64_t sb = ~uniform64(s_words[1][w]) & valid;
-        while (sb) {
-            int idx[kBatchStale];
-#pragma unroll
-            for (int u = 0; u < kBatchStale; ++u) {
-                idx[u] = sb ? (w * 64 + __builtin_ctzll(sb)) : -1;
-                sb &= sb - 1;
-            }
-            Raw8<R> raw[kBatchStale];
-#pragma unroll
-            for (int u = 0; u < kBatchStale; ++u) {
-                const int row = idx[u] >= 0 ? idx[u] : idx[0];
-                pace.stale(row);
-                load_raw<W>(reps + (int64_t)row * p.ld_r + ch.e0, ch.nv, raw[u]);
-            }
-#pragma unroll
-            for (int u = 0; u < kBatchStale; ++u) {
-                if (idx[u] >= 0) {
-                    float x[8];
-                    unpack(raw[u], x);
-                    acc.add(x, rv, ch.nv);
-                }
-            }
-        }
-    }
+    RowWalk stale(s_words[1], p.n, true, -1);
+    stream_rows<kDepthStale, R, W>(
+        reps, p.ld_r, ch, stale, [&](int row) { pace.stale(row); },
+        [&](const Raw8<R>& raw) {
+            float x[8];
+            unpack(raw, x);
+            acc.add(x, rv, ch.nv);
+        });
     acc.finish(p.n, ch.nv, pair, range);
     abs_sum = acc.abs_sum;
 }
@@ -630,7 +581,7 @@ __device__ __forceinline__ void step_chunk(const FusedParams& p, const Chunk& ch
 // latency overlaps the mask draws.
 template <class G, class R, bool DRIFT, bool W, class Pace>
 __device__ __forceinline__ void step_tile_w(const FusedParams& p, const Chunk& ch, int64_t tile,
-                                            const Pace& pace, uint64_t (*s_words)[kMaxWords]) {
+                                            Pace pace, uint64_t (*s_words)[kMaxWords]) {
     constexpr int NT = R::kPacketThreads;
     Raw8<F32> th_r, m_r, v_r;
     if (ch.nv > 0) {
@@ -639,7 +590,9 @@ __device__ __forceinline__ void step_tile_w(const FusedParams& p, const Chunk& c
         if (p.opt.kind == 2) load_raw<W>(p.v + ch.e0, ch.nv, v_r);
     }
     const int dirs[2] = {0, 1};
-    stage_masks<NT>(2, p.src, p.n, p.P, ch.k, p.step, dirs, s_words);
+    stage_masks<NT, 2>(p.src, p.n, p.P, ch.k, p.step, dirs, s_words,
+                       [&pace]() { pace.fetch(); });
+    pace.begin();
     const int nw = (p.n + 63) >> 6;
     const int K = popcount_words(s_words[0], nw);
     const int RC = popcount_words(s_words[1], nw);
@@ -709,20 +662,16 @@ __global__ void k_pace_anchor(uint64_t margin_ticks) {
 template <class G, class R, bool DRIFT>
 __global__ __launch_bounds__(R::kPacketThreads) void k_step_paced(FusedParams p, PaceParams q) {
     __shared__ uint64_t s_words[2][kMaxWords];
-    __shared__ uint64_t s_entry;
+    __shared__ uint64_t s_entry, s_anchor;
+    // Both are read after the barrier that ends the tile's mask staging.
     if (threadIdx.x == 0) s_entry = clock_ticks();
-    const uint64_t t0 =
-        __hip_atomic_load(&g_pace_anchor, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    const uint64_t r = (uint64_t)blockIdx.x / (uint64_t)q.per_round;
-    __syncthreads();
     ClockPace pace;
-    // A workgroup that starts far behind its round (its place freed late,
-    // by more than q.late) keeps the round's pace from its own start instead
-    // of rushing through the slots it missed, so that badly late workgroups
-    // stay in step with each other; smaller lateness is caught up.
-    const uint64_t nominal = t0 + ((r * q.round) >> 8);
-    const uint64_t entry = s_entry;
-    pace.base = (entry > nominal + q.late && entry - nominal < q.guard) ? entry - q.lead : nominal;
+    pace.anchor_src = &g_pace_anchor;
+    pace.anchor = &s_anchor;
+    pace.round_start = (((uint64_t)blockIdx.x / (uint64_t)q.per_round) * q.round) >> 8;
+    pace.late = q.late;
+    pace.lead = q.lead;
+    pace.entry = &s_entry;
     pace.off_g = q.off_g;
     pace.off_r = q.off_r;
     pace.off_s = q.off_s;
@@ -872,6 +821,7 @@ std::atomic<double> g_pace_lead_us{kDefaultPaceLeadUs};
 std::atomic<int> g_pace_overlap{kDefaultPaceOverlap};
 std::atomic<int> g_pace_resident{kDefaultPaceResident};
 std::atomic<double> g_pace_headroom{kDefaultPaceHeadroom};
+std::atomic<double> g_pace_tail_us{kDefaultPaceTailUs};
 
 // Compute units and clock rate of a device, and resident workgroups per
 // compute unit of a kernel, looked up once per device into fixed tables (no
@@ -919,7 +869,7 @@ int resident_per_cu(int dev, K kernel, int threads, int (&table)[kMaxDevices]) {
 PaceSetting get_pace_setting() {
     return PaceSetting{g_pace_mode.load(), g_pace_rate.load(), g_pace_gap_us.load(),
                        g_pace_lead_us.load(), g_pace_overlap.load(), g_pace_resident.load(),
-                       g_pace_headroom.load()};
+                       g_pace_headroom.load(), g_pace_tail_us.load()};
 }
 
 void set_pace_setting(const PaceSetting& st) {
@@ -930,6 +880,7 @@ void set_pace_setting(const PaceSetting& st) {
     g_pace_overlap.store(st.overlap);
     g_pace_resident.store(st.resident);
     g_pace_headroom.store(st.headroom);
+    g_pace_tail_us.store(st.tail_us);
 }
 
 // Lay out the schedule of a paced step with `tiles` tiles, or return false
@@ -945,10 +896,9 @@ void set_pace_setting(const PaceSetting& st) {
 // one round's gradient sweep runs beside the previous round's replica sweep
 // and each round's lead, gap and tail are covered by the other's streams.
 template <class G, class R, bool DRIFT>
-static bool pace_plan(const FusedParams& p, const PaceHint& h, int64_t tiles, PaceParams* q,
-                      int64_t* grid, uint64_t* margin) {
+static bool pace_plan(const PaceSetting& st, const FusedParams& p, const PaceHint& h,
+                      int64_t tiles, PaceParams* q, int64_t* grid, uint64_t* margin) {
     constexpr int NT = R::kPacketThreads;
-    const PaceSetting st = get_pace_setting();
     if (st.mode == kPaceNever || !(st.bytes_per_s > 0.0) || tiles <= 0) return false;
     int dev = 0, cus = 0;
     double tick_hz = 0.0;
@@ -983,7 +933,7 @@ static bool pace_plan(const FusedParams& p, const PaceHint& h, int64_t tiles, Pa
     const double off_s = off_r + n * dr;
     // A round's workgroups leave a little after its last slot: the last rows
     // they read must arrive and the drift partial be folded.
-    const double length = off_s + n * ds + kPaceTailUs * us;
+    const double length = off_s + n * ds + st.tail_us * us;
     // Rounds start `spacing` apart: no closer than the round's bytes at its
     // share allow with k rounds streaming (stream / k), and far enough apart
     // that a round's workgroups find places when it starts, res rounds
@@ -1019,7 +969,8 @@ static int64_t launch_fused_grd(const FusedParams& p, const PaceHint& h, hipStre
     PaceParams q;
     int64_t grid = 0;
     uint64_t margin = 0;
-    if (pace_plan<G, R, DRIFT>(pp, h, tiles, &q, &grid, &margin)) {
+    const PaceSetting st = get_pace_setting();
+    if (pace_plan<G, R, DRIFT>(st, pp, h, tiles, &q, &grid, &margin)) {
         // Bernoulli masks drawn in the step would put every workgroup's
         // draws at the start of its round, all at once; where memory for
         // them is at hand they are drawn beforehand by the mask kernel and

@@ -20,8 +20,13 @@ constexpr int kElems = 8;      // consecutive elements per thread
 constexpr int kMinPacketThreads = 128;
 constexpr int kMaxWorkers = 1024;
 constexpr int kMaxWords = kMaxWorkers / 64;
-constexpr int kBatchGrad = 4;   // gradient rows in flight per thread (aggregate)
-constexpr int kBatchStale = 4;  // stale replica rows in flight per thread (drift)
+// Row loads in flight per thread while streaming the arrived gradient rows
+// and the stale replica rows (a ring: the load of row j + depth is issued as
+// soon as row j has been used).
+constexpr int kDepthGrad = 4;
+constexpr int kDepthStale = 4;
+// Gradient rows per batch of the stale-fill estimator, which reads every row.
+constexpr int kBatchGrad = 4;
 // Replica rows in flight per thread in the standalone drift pass, which reads
 // every row: deeper batches cost occupancy (2.85 ms at 2 against 3.18 at 4 and
 // 3.82 at 8 for the 64 x 105M bf16 replicas).
@@ -258,6 +263,31 @@ __device__ __forceinline__ void store_raw(uint16_t* p, int nv, const Raw8<BF16>&
     }
 }
 
+// ---------------------------------------------------------------------------
+// Row loads through a buffer resource (CDNA buffer instructions).  The
+// resource of a row's chunk has the chunk's valid bytes as its size, so a
+// lane past the data reads zeros without touching memory, and a resource of
+// size 0 gives a load that moves nothing.  Streaming loops issue such a load
+// unconditionally on every lane, so each iteration has the same number of
+// loads in flight and the compiler waits for one row at a time instead of
+// draining every load.
+// ---------------------------------------------------------------------------
+constexpr int kBufferWord3 = 0x00020000;  // gfx9-family word 3: 32-bit data format
+
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t row_rsrc(const void* base, int bytes) {
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, bytes,
+                                             kBufferWord3);
+}
+
+__device__ __forceinline__ void load_buf(__amdgpu_buffer_rsrc_t r, int lane_bytes, Raw8<BF16>& x) {
+    x.a = __builtin_amdgcn_raw_buffer_load_b128(r, lane_bytes, 0, 0);
+}
+
+__device__ __forceinline__ void load_buf(__amdgpu_buffer_rsrc_t r, int lane_bytes, Raw8<F32>& x) {
+    x.a = __builtin_amdgcn_raw_buffer_load_b128(r, lane_bytes, 0, 0);
+    x.b = __builtin_amdgcn_raw_buffer_load_b128(r, lane_bytes + 16, 0, 0);
+}
+
 // Wave-uniform copy of a 64-bit value held identically by all active lanes.
 __device__ __forceinline__ uint64_t uniform64(uint64_t x) {
     const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)x);
@@ -285,30 +315,70 @@ __device__ __forceinline__ bool forced_arrival(int i, int64_t k, int owner,
     return i == owner || (reliable != nullptr && reliable[k] != 0);
 }
 
-// Stage the masks of packet k for `ndir` directions into words[dir][w].
-// All NT threads of the workgroup must call it (it ends with a barrier).
-template <int NT>
-__device__ __forceinline__ void stage_masks(int ndir, const MaskSource* src, int n,
-                                            int64_t num_packets, int64_t k, uint64_t step,
-                                            const int* dirs,
-                                            uint64_t (*words)[kMaxWords]) {
+// Stage the masks of packet k for NDIR directions into words[s][w]
+// (direction dirs[s] drawn from src[s]).  All NT threads of the workgroup must
+// call it (it ends with a barrier).  The source of each direction is indexed
+// by a compile-time constant, so its fields are read once per workgroup, and
+// the mask bytes of every direction are requested before any is used;
+// `fetch()` is called once by every thread right after the first requests,
+// so a load of its own overlaps them.
+struct NoFetch {
+    __device__ __forceinline__ void operator()() const {}
+};
+
+template <int NT, int NDIR, class Fetch = NoFetch>
+__device__ __forceinline__ void stage_masks(const MaskSource* src, int n, int64_t num_packets,
+                                            int64_t k, uint64_t step, const int* dirs,
+                                            uint64_t (*words)[kMaxWords],
+                                            const Fetch& fetch = Fetch()) {
     const int nw = (n + 63) >> 6;
     const int span = nw * 64;
-    for (int idx = threadIdx.x; idx < ndir * span; idx += NT) {
-        const int s = idx / span;
-        const int i = idx - s * span;
-        bool arrived = false;
-        if (i < n) {
-            if (src[s].draw)
-                arrived = bernoulli_arrived((uint64_t)k, (uint64_t)i, step, (uint64_t)dirs[s],
-                                            src[s].seed, src[s].thr);
-            else
-                arrived = src[s].mem[(int64_t)i * num_packets + k] != 0;
-            arrived = arrived || forced_arrival(i, k, src[s].owner, src[s].reliable);
+    bool rel[NDIR];
+#pragma unroll
+    for (int s = 0; s < NDIR; ++s) rel[s] = src[s].reliable != nullptr && src[s].reliable[k] != 0;
+    bool all_mem = true;
+#pragma unroll
+    for (int s = 0; s < NDIR; ++s) all_mem = all_mem && !src[s].draw;
+    auto part = [&](int base) {
+        const int i = base + (int)threadIdx.x;
+        const bool live = i < n;
+        // lanes past the last worker read worker n - 1's byte and ignore it,
+        // so that every lane issues the same loads
+        const int64_t at = (int64_t)(live ? i : n - 1) * num_packets + k;
+        uint8_t byte[NDIR];
+        if (all_mem) {
+#pragma unroll
+            for (int s = 0; s < NDIR; ++s) byte[s] = src[s].mem[at];
+        } else {
+#pragma unroll
+            for (int s = 0; s < NDIR; ++s) byte[s] = src[s].draw ? 0 : src[s].mem[at];
         }
-        const uint64_t word = __ballot(arrived);
-        if ((threadIdx.x & 63) == 0) words[s][i >> 6] = word;
-    }
+        if (base == 0) fetch();
+        bool arrived[NDIR];
+#pragma unroll
+        for (int s = 0; s < NDIR; ++s) {
+            bool a = false;
+            if (live) {
+                a = src[s].draw ? bernoulli_arrived((uint64_t)k, (uint64_t)i, step,
+                                                    (uint64_t)dirs[s], src[s].seed, src[s].thr)
+                                : byte[s] != 0;
+                a = a || i == src[s].owner || rel[s];
+            }
+            arrived[s] = a;
+        }
+        // span is a multiple of 64, so whole wavefronts take this branch
+        if (i < span) {
+#pragma unroll
+            for (int s = 0; s < NDIR; ++s) {
+                const uint64_t word = __ballot(arrived[s]);
+                if ((threadIdx.x & 63) == 0) words[s][i >> 6] = word;
+            }
+        }
+    };
+    // the first part outside the loop, so that nothing waits for the loads
+    // issued before the call
+    part(0);
+    for (int base = NT; base < span; base += NT) part(base);
     __syncthreads();
 }
 
@@ -316,6 +386,122 @@ __device__ __forceinline__ int popcount_words(const uint64_t* words, int nw) {
     int c = 0;
     for (int w = 0; w < nw; ++w) c += __popcll(uniform64(words[w]));
     return c;
+}
+
+// ---------------------------------------------------------------------------
+// Tiles of the per-packet kernels: a workgroup of NT threads owns a chunk of
+// NT * 8 elements of one packet, thread t elements e0 .. e0 + nv - 1.
+// ---------------------------------------------------------------------------
+struct Chunk {
+    int64_t k;    // packet
+    int c;        // chunk within the packet
+    int64_t c0;   // first element of the chunk
+    int cv;       // valid elements of the chunk (0 .. NT * 8)
+    int64_t e0;   // first element of this thread
+    int nv;       // valid elements of this thread (0..8)
+    bool whole;   // wave-uniform: every thread owns 0 or 8 elements, 16-byte aligned
+};
+
+// Chunk of tile b (tile = packet * cpp + chunk within the packet).  A chunk
+// is whole when it starts on a multiple of 8 elements and its valid part
+// ends on one or fills it: then every access of the tile can be a 16-byte
+// vector (row starts are 16-byte aligned).
+template <int NT>
+__device__ __forceinline__ Chunk chunk_at(int64_t b, int64_t d, int64_t L, int cpp) {
+    Chunk ch;
+    ch.k = b / cpp;
+    ch.c = (int)(b - ch.k * cpp);
+    const int64_t pk0 = ch.k * L;
+    const int64_t pend = pk0 + L < d ? pk0 + L : d;
+    ch.c0 = pk0 + (int64_t)ch.c * (NT * kElems);
+    const int64_t cv = pend - ch.c0;
+    ch.cv = cv <= 0 ? 0 : (cv >= NT * kElems ? NT * kElems : (int)cv);
+    ch.e0 = ch.c0 + (int64_t)threadIdx.x * kElems;
+    const int64_t rem = pend - ch.e0;
+    ch.nv = rem <= 0 ? 0 : (rem >= 8 ? 8 : (int)rem);
+    ch.whole = (ch.c0 % 8 == 0) && ((pend - ch.c0) % 8 == 0 || pend >= ch.c0 + NT * kElems);
+    return ch;
+}
+
+// ---------------------------------------------------------------------------
+// Streaming the rows of a packet chunk.
+// ---------------------------------------------------------------------------
+// Ascending walk over the rows whose bit is set in mask words (LDS,
+// wave-uniform) or, with `invert`, clear; row `skip` (or -1) is left out.
+// next() gives -1 after the last row.
+struct RowWalk {
+    const uint64_t* words;
+    int n, nw, w, skip;
+    bool invert;
+    uint64_t bits;
+    __device__ __forceinline__ uint64_t word(int i) const {
+        uint64_t x = uniform64(words[i]);
+        if (invert) x = ~x;
+        const int last = n - i * 64;
+        if (last < 64) x &= (1ull << last) - 1;
+        if (skip >= 0 && (skip >> 6) == i) x &= ~(1ull << (skip & 63));
+        return x;
+    }
+    __device__ __forceinline__ RowWalk(const uint64_t* words_, int n_, bool invert_, int skip_)
+        : words(words_), n(n_), nw((n_ + 63) >> 6), w(0), skip(skip_), invert(invert_) {
+        bits = nw > 0 ? word(0) : 0ull;
+    }
+    __device__ __forceinline__ int next() {
+        while (bits == 0) {
+            if (w + 1 >= nw) return -1;
+            bits = word(++w);
+        }
+        const int r = w * 64 + __builtin_ctzll(bits);
+        bits &= bits - 1;
+        return r;
+    }
+};
+
+// Hands the rows that `walk` yields, in ascending order, to use(raw) with D
+// row loads in flight per thread: the load of the row D places further on is
+// issued, after pace(row), as soon as a row has been used.  Whole tiles (W)
+// load through buffer resources; past the last row the ring issues loads of
+// size 0.  Every turn of the ring issues the same D loads and the loop is left
+// only at the end of a turn, so the compiler waits for exactly one row before
+// each use.
+template <int D, class E, bool W, class PaceFn, class UseFn>
+__device__ __forceinline__ void stream_rows(const typename E::T* rows, int64_t ld,
+                                            const Chunk& ch, RowWalk& walk, const PaceFn& pace,
+                                            const UseFn& use) {
+    const int lane = (int)threadIdx.x * kElems * (int)sizeof(typename E::T);
+    const int bytes = ch.cv * (int)sizeof(typename E::T);
+    int r[D];
+    Raw8<E> b[D];
+#pragma unroll
+    for (int u = 0; u < D; ++u) r[u] = walk.next();
+    if (r[0] < 0) return;
+    const int first = r[0];
+    auto issue = [&](int row, Raw8<E>& x) {
+        const int at = __builtin_amdgcn_readfirstlane(row >= 0 ? row : first);
+        if (W) {
+            load_buf(row_rsrc(rows + (int64_t)at * ld + ch.c0, row >= 0 ? bytes : 0), lane, x);
+        } else {
+            load_raw<false>(rows + (int64_t)at * ld + ch.e0, ch.nv, x);
+        }
+    };
+#pragma unroll
+    for (int u = 0; u < D; ++u) {
+        if (r[u] >= 0) pace(r[u]);
+        issue(r[u], b[u]);
+    }
+    for (;;) {
+#pragma unroll
+        for (int u = 0; u < D; ++u) {
+            if (r[u] >= 0) {
+                use(b[u]);
+                r[u] = walk.next();
+                if (r[u] >= 0) pace(r[u]);
+            }
+            issue(r[u], b[u]);
+        }
+        // rows are ascending: no row issued in this turn means every row is used
+        if (r[0] < 0) return;
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -330,6 +516,8 @@ __device__ __forceinline__ uint64_t clock_ticks() { return __builtin_amdgcn_s_me
 
 // Accessors without pacing (one-stage kernels and the unpaced fused step).
 struct NoPace {
+    __device__ __forceinline__ void fetch() const {}
+    __device__ __forceinline__ void begin() {}
     __device__ __forceinline__ void grad(int) const {}
     __device__ __forceinline__ void rep(int) const {}
     __device__ __forceinline__ void stale(int) const {}
@@ -340,10 +528,32 @@ struct NoPace {
 // base + off + i * delta of that sweep.  A slot further away than `guard`
 // ticks (a stale or foreign anchor) is not waited for, so every wait ends.
 struct ClockPace {
-    uint64_t base;  // round start, ticks
+    uint64_t base;  // round start, ticks (set by begin())
     uint64_t off_g, off_r, off_s;  // sweep starts, 1/256 ticks after base
     uint64_t dg, dr, ds;           // slot lengths, 1/256 ticks
     uint64_t guard;                // ticks
+    // Inputs of begin(): the schedule's anchor (read by fetch() into LDS), this
+    // round's nominal start after it, the workgroup's entry time (LDS) and
+    // the lateness rule.  fetch() and the entry time's store come before a
+    // barrier that precedes begin().
+    const uint64_t* anchor_src;
+    uint64_t* anchor;  // LDS
+    const uint64_t* entry;  // LDS
+    uint64_t round_start, late, lead;
+    __device__ __forceinline__ void fetch() const {
+        if (threadIdx.x == 0)
+            *anchor = __hip_atomic_load(anchor_src, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    // A workgroup that starts far behind its round (its place freed late, by
+    // more than `late`) keeps the round's pace from its own start instead of
+    // rushing through the slots it missed, so that badly late workgroups stay
+    // in step with each other; smaller lateness is caught up.  Called after
+    // the tile's first loads are issued, so the anchor's load overlaps them.
+    __device__ __forceinline__ void begin() {
+        const uint64_t nominal = *anchor + round_start;
+        const uint64_t e = *entry;
+        base = (e > nominal + late && e - nominal < guard) ? e - lead : nominal;
+    }
     __device__ __forceinline__ void at(uint64_t off, uint64_t delta, int i) const {
         const uint64_t t = base + ((off + (uint64_t)i * delta) >> 8);
         uint64_t now = clock_ticks();
@@ -414,11 +624,13 @@ __device__ __forceinline__ float parity_invq(const AggVariant& v, int64_t k, int
 // arrived value or, if lost, its last arrived one from g_prev; arrived values
 // are written to g_prev; g = sum / n.
 template <class E, bool W, class Pace>
-__device__ __forceinline__ void aggregate8(const typename E::T* grads, int64_t ld,
-                                           int64_t e0, int nv, const uint64_t* gm, int nw,
-                                           int n, int K, float lam, const float (&th)[8],
-                                           const AggVariant& var, bool reliable_packet,
-                                           const Pace& pace, float (&g)[8]) {
+__device__ __forceinline__ void aggregate8(const typename E::T* grads, int64_t ld, const Chunk& ch,
+                                           const uint64_t* gm, int n, int K, float lam,
+                                           const float (&th)[8], const AggVariant& var,
+                                           bool reliable_packet, const Pace& pace,
+                                           float (&g)[8]) {
+    const int64_t e0 = ch.e0;
+    const int nv = ch.nv;
 #pragma unroll
     for (int j = 0; j < 8; ++j) g[j] = 0.0f;
     if (var.kind == kEstStaleFill) {
@@ -452,34 +664,15 @@ __device__ __forceinline__ void aggregate8(const typename E::T* grads, int64_t l
     }
     const bool ht = var.kind == kEstHorvitzThompson;
     const int sure_row = (ht && !reliable_packet) ? var.owner : -1;
-    for (int w = 0; w < nw; ++w) {
-        uint64_t bits = uniform64(gm[w]);
-        if (sure_row >= 0 && (sure_row >> 6) == w) bits &= ~(1ull << (sure_row & 63));
-        while (bits) {
-            int idx[kBatchGrad];
+    RowWalk walk(gm, n, false, sure_row);
+    stream_rows<kDepthGrad, E, W>(
+        grads, ld, ch, walk, [&](int row) { pace.grad(row); },
+        [&](const Raw8<E>& raw) {
+            float x[8];
+            unpack(raw, x);
 #pragma unroll
-            for (int u = 0; u < kBatchGrad; ++u) {
-                idx[u] = bits ? (w * 64 + __builtin_ctzll(bits)) : -1;
-                bits &= bits - 1;  // no-op once bits == 0
-            }
-            Raw8<E> raw[kBatchGrad];
-#pragma unroll
-            for (int u = 0; u < kBatchGrad; ++u) {
-                const int row = idx[u] >= 0 ? idx[u] : idx[0];
-                pace.grad(row);
-                load_raw<W>(grads + (int64_t)row * ld + e0, nv, raw[u]);
-            }
-#pragma unroll
-            for (int u = 0; u < kBatchGrad; ++u) {
-                if (idx[u] >= 0) {
-                    float x[8];
-                    unpack(raw[u], x);
-#pragma unroll
-                    for (int j = 0; j < 8; ++j) g[j] += x[j];
-                }
-            }
-        }
-    }
+            for (int j = 0; j < 8; ++j) g[j] += x[j];
+        });
     if (ht) {
         const float nf = (float)n;
         if (reliable_packet) {
