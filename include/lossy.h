@@ -376,10 +376,9 @@ LL_API int lossy_step_fused_noalloc(int32_t n, int64_t d, int64_t packet, uint64
  *                when it starts.
  *   headroom     fraction of those places the rounds fill ((0, 1]; 1.0).
  *   tail_us      time after a round's last slot before the next round may
- *                count on its places ([0, 1e4]; default 2.5).
- * A workgroup that starts more than 10 us behind its round (its place freed
- * late) keeps the round's pace from its own start rather than rushing
- * through the slots it missed; smaller lateness is caught up.
+ *                count on its places ([0, 1e4]; default 3).
+ * A workgroup that starts behind its round (its place freed late) issues the
+ * rows whose slots have passed at once and then keeps the round's slots.
  * The setting is process-wide and read at each call.  A paced step enqueues,
  * before the step itself: the Bernoulli mask kernel for each direction whose
  * masks have memory to go to (the caller's mask output, else the workspace

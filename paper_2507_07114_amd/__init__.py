@@ -241,7 +241,7 @@ PACE_MODES = {"auto": 0, "always": 1, "never": 2}
 
 def ll_set_pacing(mode: str = "auto", bytes_per_s: float = 6.25e12, gap_us: float = 2.0,
                   lead_us: float = 4.0, overlap: int = 1, resident: int = 1,
-                  headroom: float = 1.0, tail_us: float = 2.5) -> None:
+                  headroom: float = 1.0, tail_us: float = 3.0) -> None:
     """Process-wide pacing of lossy_step_fused (a performance setting; see
     include/lossy.h)."""
     if mode not in PACE_MODES:

@@ -149,8 +149,6 @@ struct PaceParams {
     uint64_t off_g, off_r, off_s;  // gradient, replica and stale-read sweep starts
     uint64_t dg, dr, ds;           // slot lengths of the three sweeps
     uint64_t guard;                // longest wait, ticks
-    uint64_t lead;                 // lead of a round, ticks
-    uint64_t late;                 // lateness past which a workgroup keeps its own pace, ticks
 };
 
 // Pacing modes and defaults: auto paces steps of bf16 rows, at least
@@ -167,9 +165,7 @@ constexpr double kDefaultPaceLeadUs = 4.0;
 constexpr int kDefaultPaceOverlap = 1;
 constexpr int kDefaultPaceResident = 1;
 constexpr double kPaceMarginUs = 3.0;
-constexpr double kDefaultPaceTailUs = 2.5;
-// Lateness past which a workgroup keeps its round's pace from its own start.
-constexpr double kPaceLateUs = 10.0;
+constexpr double kDefaultPaceTailUs = 3.0;
 // Fraction of the resident workgroup places the rounds in flight may fill.
 constexpr double kDefaultPaceHeadroom = 1.0;
 

@@ -662,16 +662,11 @@ __global__ void k_pace_anchor(uint64_t margin_ticks) {
 template <class G, class R, bool DRIFT>
 __global__ __launch_bounds__(R::kPacketThreads) void k_step_paced(FusedParams p, PaceParams q) {
     __shared__ uint64_t s_words[2][kMaxWords];
-    __shared__ uint64_t s_entry, s_anchor;
-    // Both are read after the barrier that ends the tile's mask staging.
-    if (threadIdx.x == 0) s_entry = clock_ticks();
+    __shared__ uint64_t s_anchor;  // read after the barrier that ends the mask staging
     ClockPace pace;
     pace.anchor_src = &g_pace_anchor;
     pace.anchor = &s_anchor;
     pace.round_start = (((uint64_t)blockIdx.x / (uint64_t)q.per_round) * q.round) >> 8;
-    pace.late = q.late;
-    pace.lead = q.lead;
-    pace.entry = &s_entry;
     pace.off_g = q.off_g;
     pace.off_r = q.off_r;
     pace.off_s = q.off_s;
@@ -944,8 +939,6 @@ static bool pace_plan(const PaceSetting& st, const FusedParams& p, const PaceHin
     const double spacing = stream / k > length / res ? stream / k : length / res;
     if (!(length < 1e15)) return false;
     q->per_round = g;
-    q->lead = (uint64_t)(st.lead_us * 1e-6 * tick_hz);
-    q->late = (uint64_t)(kPaceLateUs * 1e-6 * tick_hz);
     q->dg = (uint64_t)dg;
     q->dr = (uint64_t)dr;
     q->ds = (uint64_t)ds;

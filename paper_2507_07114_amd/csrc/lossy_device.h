@@ -532,34 +532,32 @@ struct ClockPace {
     uint64_t off_g, off_r, off_s;  // sweep starts, 1/256 ticks after base
     uint64_t dg, dr, ds;           // slot lengths, 1/256 ticks
     uint64_t guard;                // ticks
-    // Inputs of begin(): the schedule's anchor (read by fetch() into LDS), this
-    // round's nominal start after it, the workgroup's entry time (LDS) and
-    // the lateness rule.  fetch() and the entry time's store come before a
-    // barrier that precedes begin().
+    // Inputs of begin(): the schedule's anchor (read by fetch() into LDS
+    // before a barrier that precedes begin()) and this round's start after it.
     const uint64_t* anchor_src;
     uint64_t* anchor;  // LDS
-    const uint64_t* entry;  // LDS
-    uint64_t round_start, late, lead;
+    uint64_t round_start;
     __device__ __forceinline__ void fetch() const {
         if (threadIdx.x == 0)
             *anchor = __hip_atomic_load(anchor_src, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
-    // A workgroup that starts far behind its round (its place freed late, by
-    // more than `late`) keeps the round's pace from its own start instead of
-    // rushing through the slots it missed, so that badly late workgroups stay
-    // in step with each other; smaller lateness is caught up.  Called after
-    // the tile's first loads are issued, so the anchor's load overlaps them.
-    __device__ __forceinline__ void begin() {
-        const uint64_t nominal = *anchor + round_start;
-        const uint64_t e = *entry;
-        base = (e > nominal + late && e - nominal < guard) ? e - lead : nominal;
-    }
+    // Every workgroup keeps its round's slots: one that starts late issues the
+    // rows whose slots have passed at once and then follows the schedule.
+    // Called after the tile's first loads are issued, so the anchor's load
+    // overlaps them.
+    __device__ __forceinline__ void begin() { base = *anchor + round_start; }
     __device__ __forceinline__ void at(uint64_t off, uint64_t delta, int i) const {
         const uint64_t t = base + ((off + (uint64_t)i * delta) >> 8);
         uint64_t now = clock_ticks();
         if (t <= now || t - now > guard) return;
+        // every waiting wave reads the shared clock; far from the slot it
+        // sleeps longer between reads (s_sleep n: about 64 n core clocks,
+        // 27 n ns at 2.4 GHz, so no sleep overshoots the slot)
         while (now < t) {
-            __builtin_amdgcn_s_sleep(1);
+            const uint64_t rem = t - now;
+            if (rem > 100) __builtin_amdgcn_s_sleep(16);
+            else if (rem > 20) __builtin_amdgcn_s_sleep(4);
+            else __builtin_amdgcn_s_sleep(1);
             now = clock_ticks();
         }
     }
