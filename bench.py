@@ -14,7 +14,7 @@ Throughput is algorithmic HBM bytes per second: arrived gradient packets
 read, master + moments read and written, arrived replica packets written
 and, for drift, stale replica packets read (lost gradient packets are never
 needed, so never counted).  Prints one JSON line on stdout.  Workloads
-smaller than 1 GiB get a 1 GiB scratch fill between timed steps so that
+smaller than 1 GiB get a 1 GiB scratch read between timed steps so that
 they are not served from the 256 MB memory-side cache; their throughput is
 then taken over the per-step events.
 """
@@ -86,9 +86,10 @@ def algorithmic_bytes(w, mg, mb, lens, drift: bool, estimator: str = "arrived_me
     return out
 
 
-def read_pmc_traffic(expect_hash: str):
+def read_pmc_traffic(expect_hash: str, workload: str):
     """HBM bytes per dispatch from the committed rocprofv3 counter summary, or
-    None when it is absent or was taken on different kernel sources."""
+    None when it is absent, was taken on different kernel sources or on
+    another workload."""
     if not os.path.exists(PMC_PROFILE):
         return None
     vals = {}
@@ -97,7 +98,7 @@ def read_pmc_traffic(expect_hash: str):
             if ":" in line and not line.startswith("#"):
                 k, v = line.split(":", 1)
                 vals[k.strip()] = v.strip()
-    if vals.get("kernel_source_sha256") != expect_hash:
+    if vals.get("kernel_source_sha256") != expect_hash or vals.get("workload") != workload:
         return None
     try:
         return float(vals["hbm_bytes_per_dispatch"])
@@ -252,6 +253,9 @@ def main():
     ap.add_argument("--ages", action="store_true", help="track broadcast ages")
     ap.add_argument("--parity-group", type=int, default=0,
                     help="packets per XOR parity packet (0: no parity packets)")
+    ap.add_argument("--mall-flush", choices=("read", "write"), default="read",
+                    help="how a 1 GiB buffer evicts small workloads from the memory-side "
+                         "cache between timed steps")
     ap.add_argument("--stagewise", action="store_true",
                     help="time the chain of one-stage entry points (ll_masks, lossy_aggregate, "
                          "shard_step, lossy_broadcast, drift_stats) instead of the fused step")
@@ -360,12 +364,21 @@ def main():
 
     # A workload smaller than the 256 MB memory-side cache (MALL) would be
     # served from it on every step after the first: for footprints under
-    # 1 GiB a 1 GiB scratch fill runs between steps, outside the timed
-    # events, and the throughput is taken over the events alone.
+    # 1 GiB a 1 GiB scratch buffer streams through the cache between steps,
+    # outside the timed events, and the throughput is taken over the events
+    # alone.  By default the buffer is read (the hand-written read probe), so
+    # the cache is left holding clean lines; written ("write"), it is left
+    # holding dirty lines that the timed step then has to write back.
     footprint = sum(t.numel() * t.element_size()
                     for t in (dev.grads, dev.replicas, dev.theta, dev.m, dev.v) if t is not None)
     mall_flush = footprint < (1 << 30)
-    scratch = torch.empty(1 << 28, dtype=torch.float32, device="cuda") if mall_flush else None
+    scratch = torch.zeros(1 << 28, dtype=torch.float32, device="cuda") if mall_flush else None
+    if mall_flush and args.mall_flush == "read":
+        from paper_2507_07114_amd import probe
+        sink = torch.zeros(probe.SINK_BYTES, dtype=torch.uint8, device="cuda")
+        flush = lambda j: probe.hbm_probe_read(scratch, sink)
+    else:
+        flush = lambda j: scratch.fill_(float(j))
 
     stream = torch.cuda.current_stream()
     starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
@@ -374,7 +387,7 @@ def main():
     wall0 = time.perf_counter()
     for j in range(args.steps):
         if mall_flush:
-            scratch.fill_(float(j))
+            flush(j)
         starts[j].record(stream)
         step_fn(args.warmup + j)
         ends[j].record(stream)
@@ -398,7 +411,8 @@ def main():
     launch_ms = float(np.mean(ms))
     achieved = mean_bytes / (launch_ms * 1e-3) / 1e9
     khash = kernel_source_hash()
-    traffic = None if args.stagewise else read_pmc_traffic(khash)
+    # the counters were taken on the plain fused step of one workload
+    traffic = None if (args.stagewise or variant) else read_pmc_traffic(khash, w.name)
     mean_b = {k: int(np.mean([b[k] for b in per_step_bytes])) for k in per_step_bytes[0]}
     log(f"per-launch event times (ms): min {min(ms):.3f} median {float(np.median(ms)):.3f} "
         f"max {max(ms):.3f}; algorithmic bytes/step {mean_b}")
@@ -424,7 +438,7 @@ def main():
                    "reliable_every": args.reliable_every, "ages": args.ages,
                    "parity_group": args.parity_group, "stagewise": args.stagewise,
                    "footprint_bytes": footprint,
-                   "mall_flush_between_steps": mall_flush},
+                   "mall_flush_between_steps": (args.mall_flush if mall_flush else False)},
         "pct_hbm_peak": round(100.0 * value / HBM_PEAK_GBS, 2),
         "elements_per_s": round(w.n * w.d / (ms_per_step * 1e-3), 1),
         "shard_elements_per_s": round(w.d / (ms_per_step * 1e-3), 1),

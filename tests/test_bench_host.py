@@ -55,3 +55,15 @@ def test_more_than_one_gpu_is_refused():
                        capture_output=True, text=True, timeout=120)
     assert r.returncode == 2
     assert "one GPU" in r.stderr and r.stdout == ""
+
+
+def test_counter_traffic_only_for_its_workload_and_sources(tmp_path, monkeypatch):
+    prof = tmp_path / "pmc.txt"
+    prof.write_text("# header: comment lines are skipped\nkernel_source_sha256: abc\n"
+                    "workload: n64_llama7b_shard_bf16_adam\nhbm_bytes_per_dispatch: 123\n")
+    monkeypatch.setattr(bench, "PMC_PROFILE", str(prof))
+    assert bench.read_pmc_traffic("abc", "n64_llama7b_shard_bf16_adam") == 123.0
+    assert bench.read_pmc_traffic("abd", "n64_llama7b_shard_bf16_adam") is None
+    assert bench.read_pmc_traffic("abc", "n8_d16m_bf16_adam") is None
+    monkeypatch.setattr(bench, "PMC_PROFILE", str(tmp_path / "missing.txt"))
+    assert bench.read_pmc_traffic("abc", "n64_llama7b_shard_bf16_adam") is None
