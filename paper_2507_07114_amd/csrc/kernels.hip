@@ -476,10 +476,11 @@ __global__ __launch_bounds__(kThreads) void k_drift_reduce(const DriftPartial* p
 }
 
 // Up to kDirectFold partials: one workgroup of kFoldThreads folds them
-// directly, in a fixed order, each thread with eight loads in flight (N = 8
-// step, 8192 partials: 8.2 us, against 10.2 us for two levels; 1024 threads
-// took as long).
-constexpr int kFoldThreads = 256;
+// directly, in a fixed order, each thread with kFoldDepth loads in flight, so
+// that up to kFoldThreads * kFoldDepth partials (the N = 8 step's 8192) take
+// one memory round trip.
+constexpr int kFoldThreads = 512;
+constexpr int kFoldDepth = 16;
 constexpr int64_t kDirectFold = 16384;
 
 __global__ __launch_bounds__(kFoldThreads) void k_drift_direct(const DriftPartial* parts,
@@ -487,14 +488,26 @@ __global__ __launch_bounds__(kFoldThreads) void k_drift_direct(const DriftPartia
                                                                int have_master, DriftOut* out) {
     DriftAcc a;
     a.zero();
-    // thread t folds partials j = t, t + kFoldThreads, ... in order
+    // thread t folds partials j = t, t + kFoldThreads, ... in order; each
+    // batch of kFoldDepth partials is requested (two 16-byte loads each; the
+    // partials are 32 bytes, 32-byte aligned) before any is used
+    static_assert(sizeof(DriftPartial) == 32, "two 16-byte loads per partial");
+    union Raw {
+        u32x4 v[2];
+        DriftPartial q;
+    };
+    const u32x4* pv = reinterpret_cast<const u32x4*>(parts);
     int64_t j = threadIdx.x;
-    for (; j + 7 * kFoldThreads < count; j += 8 * kFoldThreads) {
-        DriftPartial q[8];
+    for (; j + (kFoldDepth - 1) * kFoldThreads < count; j += kFoldDepth * kFoldThreads) {
+        Raw q[kFoldDepth];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) q[u] = parts[j + u * kFoldThreads];
+        for (int u = 0; u < kFoldDepth; ++u) {
+            q[u].v[0] = pv[2 * (j + u * kFoldThreads)];
+            q[u].v[1] = pv[2 * (j + u * kFoldThreads) + 1];
+        }
+        __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-        for (int u = 0; u < 8; ++u) a.add(q[u]);
+        for (int u = 0; u < kFoldDepth; ++u) a.add(q[u].q);
     }
     for (; j < count; j += kFoldThreads) a.add(parts[j]);
     const DriftAcc t = block_fold<kFoldThreads>(a);
