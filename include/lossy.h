@@ -377,6 +377,13 @@ LL_API int lossy_step_fused_noalloc(int32_t n, int64_t d, int64_t packet, uint64
  *   headroom     fraction of those places the rounds fill ((0, 1]; 1.0).
  *   tail_us      time after a round's last slot before the next round may
  *                count on its places ([0, 1e4]; default 3).
+ *   persistent   1: steps in the plain configuration (arrived-mean
+ *                estimator, masks drawn beforehand or from memory, no forced
+ *                arrivals, ages or mask outputs beyond the drawn masks,
+ *                packet length and shard a multiple of 8) run one round's
+ *                worth of workgroups that loop over the rounds, so no
+ *                workgroup starts or leaves between rounds; needs overlap
+ *                and resident 1.  0: one workgroup per tile (default 0).
  * A workgroup that starts behind its round (its place freed late) issues the
  * rows whose slots have passed at once and then keeps the round's slots.
  * The setting is process-wide and read at each call.  A paced step enqueues,
@@ -389,7 +396,7 @@ LL_API int lossy_step_fused_noalloc(int32_t n, int64_t d, int64_t packet, uint64
  * other's start time, which costs speed but changes no result.
  * ll_set_pacing returns LL_EINVAL for an unknown mode or a field outside the
  * ranges above (bytes_per_s in (0, 1e15), gap_us, lead_us and tail_us in
- * [0, 1e4]);
+ * [0, 1e4], persistent 0 or 1 and only with overlap and resident 1);
  * ll_get_pacing fills `out` (host).
  */
 enum { LL_PACE_AUTO = 0, LL_PACE_ALWAYS = 1, LL_PACE_NEVER = 2 };
@@ -402,6 +409,7 @@ typedef struct {
     int32_t resident;
     double headroom;
     double tail_us;
+    int32_t persistent;
 } ll_pacing;
 
 LL_API int ll_set_pacing(const ll_pacing* cfg);

@@ -346,8 +346,13 @@ int ll_set_pacing(const ll_pacing* cfg) {
         return fail(LL_EINVAL, "headroom must lie in (0, 1]");
     if (!(cfg->tail_us >= 0.0 && cfg->tail_us <= 1e4))
         return fail(LL_EINVAL, "tail_us must lie in [0, 1e4]");
+    if (cfg->persistent != 0 && cfg->persistent != 1)
+        return fail(LL_EINVAL, "persistent=%d must be 0 or 1", cfg->persistent);
+    if (cfg->persistent && (cfg->overlap != 1 || cfg->resident != 1))
+        return fail(LL_EINVAL, "persistent pacing needs overlap=1 and resident=1");
     set_pace_setting(PaceSetting{cfg->mode, cfg->bytes_per_s, cfg->gap_us, cfg->lead_us,
-                                 cfg->overlap, cfg->resident, cfg->headroom, cfg->tail_us});
+                                 cfg->overlap, cfg->resident, cfg->headroom, cfg->tail_us,
+                                 cfg->persistent});
     return ok();
 }
 
@@ -362,6 +367,7 @@ int ll_get_pacing(ll_pacing* out) {
     out->resident = st.resident;
     out->headroom = st.headroom;
     out->tail_us = st.tail_us;
+    out->persistent = st.persistent;
     return ok();
 }
 

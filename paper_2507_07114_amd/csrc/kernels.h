@@ -166,6 +166,7 @@ constexpr int kDefaultPaceOverlap = 1;
 constexpr int kDefaultPaceResident = 1;
 constexpr double kPaceMarginUs = 3.0;
 constexpr double kDefaultPaceTailUs = 3.0;
+constexpr int kDefaultPacePersistent = 0;
 // Fraction of the resident workgroup places the rounds in flight may fill.
 constexpr double kDefaultPaceHeadroom = 1.0;
 
@@ -179,6 +180,7 @@ struct PaceSetting {
     int resident;        // rounds the resident workgroup places are shared by (>= overlap)
     double headroom;     // fraction of the resident places the rounds may fill
     double tail_us;      // allowance after a round's last slot
+    int persistent;      // 1: one round of workgroups loops over the rounds (plain steps)
 };
 PaceSetting get_pace_setting();
 void set_pace_setting(const PaceSetting& s);

@@ -690,6 +690,145 @@ __global__ __launch_bounds__(R::kPacketThreads) void k_step_paced(FusedParams p,
     step_tile<G, R, DRIFT>(p, blockIdx.x, pace, s_words);
 }
 
+// ---------------------------------------------------------------------------
+// Persistent paced step for the plain configuration: arrived-mean estimator,
+// no forced arrivals, ages or mask outputs, both directions' masks already in
+// memory, whole tiles only (packet length and shard a multiple of 8).
+// per_round workgroups loop over the rounds, workgroup b doing tile
+// r * per_round + b in round r, so no workgroup starts or leaves between
+// rounds.  The tile body is its own (no variant paths), so the loop carries
+// nothing but the loop itself.
+// ---------------------------------------------------------------------------
+template <int NT>
+__device__ __forceinline__ void stage_masks_mem2(const uint8_t* mem_g, const uint8_t* mem_b,
+                                                 int n, int64_t P, int64_t k,
+                                                 const ClockPace& pace,
+                                                 uint64_t (*words)[kMaxWords]) {
+    const int span = ((n + 63) >> 6) * 64;
+    for (int base = 0; base < span; base += NT) {
+        const int i = base + (int)threadIdx.x;
+        const bool live = i < n;
+        const int64_t at = (int64_t)(live ? i : n - 1) * P + k;
+        const uint8_t bg = mem_g[at], bb = mem_b[at];
+        if (base == 0) pace.fetch();
+        if (i < span) {
+            const uint64_t wg = __ballot(live && bg != 0);
+            const uint64_t wb = __ballot(live && bb != 0);
+            if ((threadIdx.x & 63) == 0) {
+                words[0][i >> 6] = wg;
+                words[1][i >> 6] = wb;
+            }
+        }
+    }
+    __syncthreads();
+}
+
+template <class G, class R, bool DRIFT>
+__device__ __forceinline__ void lean_tile(const FusedParams& p, int64_t tile, ClockPace& pace,
+                                          uint64_t (*s_words)[kMaxWords]) {
+    constexpr int NT = R::kPacketThreads;
+    const Chunk ch = chunk_at<NT>(tile, p.d, p.L, p.cpp);
+    Raw8<F32> th_r, m_r, v_r;
+    if (ch.nv > 0) {
+        load_chunk<true>(p.theta, ch, th_r);
+        if (p.opt.kind >= 1) load_chunk<true>(p.m, ch, m_r);
+        if (p.opt.kind == 2) load_chunk<true>(p.v, ch, v_r);
+    }
+    stage_masks_mem2<NT>(p.src[0].mem, p.src[1].mem, p.n, p.P, ch.k, pace, s_words);
+    pace.begin();
+    const int nw = (p.n + 63) >> 6;
+    const int K = popcount_words(s_words[0], nw);
+    const int RC = popcount_words(s_words[1], nw);
+    if (ch.c == 0 && threadIdx.x == 0 && p.counts) p.counts[ch.k] = K;
+    double pair = 0.0, range = 0.0, abs_sum = 0.0;
+    if (ch.nv > 0) {
+        float th[8], mm[8], vv[8], g[8];
+        unpack(th_r, th);
+#pragma unroll
+        for (int j = 0; j < 8; ++j) g[j] = 0.0f;
+        RowWalk walk(s_words[0], p.n, false, -1);
+        stream_rows<kDepthGrad, G, true>(
+            reinterpret_cast<const typename G::T*>(p.grads), p.ld_g, ch, walk,
+            [&](int row) { pace.grad(row); },
+            [&](const Raw8<G>& raw) {
+                float x[8];
+                unpack(raw, x);
+#pragma unroll
+                for (int j = 0; j < 8; ++j) g[j] += x[j];
+            });
+        if (K > 0) {
+            const float kf = (float)K;
+#pragma unroll
+            for (int j = 0; j < 8; ++j) g[j] = g[j] / kf;
+        } else {
+#pragma unroll
+            for (int j = 0; j < 8; ++j) g[j] = p.lam * th[j];
+        }
+        if (p.opt.kind >= 1) unpack(m_r, mm);
+        if (p.opt.kind == 2) unpack(v_r, vv);
+        update8(p.opt, th, mm, vv, g);
+        store_chunk<true>(p.theta, ch, th);
+        if (p.opt.kind >= 1) store_chunk<true>(p.m, ch, mm);
+        if (p.opt.kind == 2) store_chunk<true>(p.v, ch, vv);
+        Packed8<R> r;
+        r.pack(th);
+        typename R::T* reps = reinterpret_cast<typename R::T*>(p.replicas);
+        RowWalk arrived(s_words[1], p.n, false, -1);
+        for (int i = arrived.next(); i >= 0; i = arrived.next()) {
+            pace.rep(i);
+            store_chunk<true>(reps + (int64_t)i * p.ld_r, ch, r);
+        }
+        if (DRIFT) {
+            Drift8 acc;
+            float rv[8];
+#pragma unroll
+            for (int j = 0; j < 8; ++j) rv[j] = r.value(j);
+            acc.init(RC > 0, rv);
+            RowWalk stale(s_words[1], p.n, true, -1);
+            stream_rows<kDepthStale, R, true>(
+                reps, p.ld_r, ch, stale, [&](int row) { pace.stale(row); },
+                [&](const Raw8<R>& raw) {
+                    float x[8];
+                    unpack(raw, x);
+                    acc.add(x, rv, ch.nv);
+                });
+            acc.finish(p.n, ch.nv, pair, range);
+            abs_sum = acc.abs_sum;
+        }
+    }
+    if (DRIFT) {
+        const uint32_t stale = ch.c == 0 ? (uint32_t)(p.n - RC) : 0u;
+        const uint32_t empty = (ch.c == 0 && K == 0) ? 1u : 0u;
+        block_reduce_partial<NT>(pair, abs_sum, range, stale, empty, p.partials + tile);
+        if (tile == 0 && threadIdx.x == 0) *reduce_counter(p.groups) = 0u;
+    }
+}
+
+template <class G, class R, bool DRIFT>
+__global__ __launch_bounds__(R::kPacketThreads) void k_step_lean(FusedParams p, PaceParams q,
+                                                                 int64_t tiles) {
+    __shared__ uint64_t s_words[2][kMaxWords];
+    __shared__ uint64_t s_anchor;
+    for (int64_t r = 0;; ++r) {
+        const int64_t tile = r * q.per_round + (int64_t)blockIdx.x;
+        if (tile >= tiles) break;
+        ClockPace pace;
+        pace.anchor_src = &g_pace_anchor;
+        pace.anchor = &s_anchor;
+        pace.round_start = ((uint64_t)r * q.round) >> 8;
+        pace.off_g = q.off_g;
+        pace.off_r = q.off_r;
+        pace.off_s = q.off_s;
+        pace.dg = q.dg;
+        pace.dr = q.dr;
+        pace.ds = q.ds;
+        pace.guard = q.guard;
+        lean_tile<G, R, DRIFT>(p, tile, pace, s_words);
+        // the next tile rewrites the masks and the anchor in LDS
+        __syncthreads();
+    }
+}
+
 __global__ void k_drift_zero(DriftOut* out) {
     if (threadIdx.x == 0) {
         DriftOut r;
@@ -830,6 +969,7 @@ std::atomic<int> g_pace_overlap{kDefaultPaceOverlap};
 std::atomic<int> g_pace_resident{kDefaultPaceResident};
 std::atomic<double> g_pace_headroom{kDefaultPaceHeadroom};
 std::atomic<double> g_pace_tail_us{kDefaultPaceTailUs};
+std::atomic<int> g_pace_persistent{kDefaultPacePersistent};
 
 // Compute units and clock rate of a device, and resident workgroups per
 // compute unit of a kernel, looked up once per device into fixed tables (no
@@ -877,7 +1017,7 @@ int resident_per_cu(int dev, K kernel, int threads, int (&table)[kMaxDevices]) {
 PaceSetting get_pace_setting() {
     return PaceSetting{g_pace_mode.load(), g_pace_rate.load(), g_pace_gap_us.load(),
                        g_pace_lead_us.load(), g_pace_overlap.load(), g_pace_resident.load(),
-                       g_pace_headroom.load(), g_pace_tail_us.load()};
+                       g_pace_headroom.load(), g_pace_tail_us.load(), g_pace_persistent.load()};
 }
 
 void set_pace_setting(const PaceSetting& st) {
@@ -889,6 +1029,7 @@ void set_pace_setting(const PaceSetting& st) {
     g_pace_resident.store(st.resident);
     g_pace_headroom.store(st.headroom);
     g_pace_tail_us.store(st.tail_us);
+    g_pace_persistent.store(st.persistent);
 }
 
 // Lay out the schedule of a paced step with `tiles` tiles, or return false
@@ -904,15 +1045,16 @@ void set_pace_setting(const PaceSetting& st) {
 // one round's gradient sweep runs beside the previous round's replica sweep
 // and each round's lead, gap and tail are covered by the other's streams.
 template <class G, class R, bool DRIFT>
-static bool pace_plan(const PaceSetting& st, const FusedParams& p, const PaceHint& h,
+static bool pace_plan(const PaceSetting& st, bool lean, const FusedParams& p, const PaceHint& h,
                       int64_t tiles, PaceParams* q, int64_t* grid, uint64_t* margin) {
     constexpr int NT = R::kPacketThreads;
     if (st.mode == kPaceNever || !(st.bytes_per_s > 0.0) || tiles <= 0) return false;
     int dev = 0, cus = 0;
     double tick_hz = 0.0;
     if (hipGetDevice(&dev) != hipSuccess || !device_info(dev, &cus, &tick_hz)) return false;
-    static int occupancy[kMaxDevices];
-    const int per_cu = resident_per_cu(dev, k_step_paced<G, R, DRIFT>, NT, occupancy);
+    static int occupancy[kMaxDevices], occupancy_lean[kMaxDevices];
+    const int per_cu = lean ? resident_per_cu(dev, k_step_lean<G, R, DRIFT>, NT, occupancy_lean)
+                            : resident_per_cu(dev, k_step_paced<G, R, DRIFT>, NT, occupancy);
     const int k = st.overlap < 1 ? 1 : (st.overlap > 2 ? 2 : st.overlap);
     const int res = st.resident < k ? k : st.resident;
     const int64_t gmax = (int64_t)(st.headroom * per_cu * cus / res);
@@ -976,26 +1118,36 @@ static int64_t launch_fused_grd(const FusedParams& p, const PaceHint& h, hipStre
     int64_t grid = 0;
     uint64_t margin = 0;
     const PaceSetting st = get_pace_setting();
-    if (pace_plan<G, R, DRIFT>(st, pp, h, tiles, &q, &grid, &margin)) {
-        // Bernoulli masks drawn in the step would put every workgroup's
-        // draws at the start of its round, all at once; where memory for
-        // them is at hand they are drawn beforehand by the mask kernel and
-        // the step reads them.
-        MaskJob jobs[2];
-        int njobs = 0;
-        for (int dir = 0; dir < 2; ++dir) {
-            if (!pp.src[dir].draw || !pp.pre[dir]) continue;
-            const MaskSource& m = pp.src[dir];
-            jobs[njobs++] = MaskJob{(uint64_t)dir, m.seed, m.thr, m.owner, m.reliable, pp.pre[dir]};
-            pp.src[dir] = MaskSource{false, 0, 0, pp.pre[dir], -1, nullptr};
-            if (dir == 0 && pp.out_g == pp.pre[0]) pp.out_g = nullptr;
-            if (dir == 1 && pp.out_b == pp.pre[1]) pp.out_b = nullptr;
-        }
-        if (njobs && launch_masks_bernoulli_jobs(pp.n, pp.P, pp.step, jobs, njobs, s) != hipSuccess)
+    // Bernoulli masks drawn in the step would put every workgroup's draws at
+    // the start of its round, all at once; a paced step has them drawn
+    // beforehand by the mask kernel, where memory for them is at hand, and
+    // reads them.
+    FusedParams pm = pp;
+    MaskJob jobs[2];
+    int njobs = 0;
+    for (int dir = 0; dir < 2; ++dir) {
+        if (!pm.src[dir].draw || !pm.pre[dir]) continue;
+        const MaskSource& m = pm.src[dir];
+        jobs[njobs++] = MaskJob{(uint64_t)dir, m.seed, m.thr, m.owner, m.reliable, pm.pre[dir]};
+        pm.src[dir] = MaskSource{false, 0, 0, pm.pre[dir], -1, nullptr};
+        if (dir == 0 && pm.out_g == pm.pre[0]) pm.out_g = nullptr;
+        if (dir == 1 && pm.out_b == pm.pre[1]) pm.out_b = nullptr;
+    }
+    // The persistent form takes the plain configuration only (see k_step_lean).
+    bool lean = st.persistent && pm.var.kind == kEstArrivedMean && !pm.ages && !pm.out_g &&
+                !pm.out_b && pm.L % 8 == 0 && pm.d % 8 == 0;
+    for (int dir = 0; dir < 2; ++dir)
+        lean = lean && !pm.src[dir].draw && pm.src[dir].owner < 0 && !pm.src[dir].reliable;
+    if (pace_plan<G, R, DRIFT>(st, lean, pm, h, tiles, &q, &grid, &margin)) {
+        if (njobs && launch_masks_bernoulli_jobs(pm.n, pm.P, pm.step, jobs, njobs, s) != hipSuccess)
             return -1;
         hipLaunchKernelGGL(k_pace_anchor, dim3(1), dim3(64), 0, s, margin);
-        hipLaunchKernelGGL((k_step_paced<G, R, DRIFT>), dim3((unsigned)tiles), dim3(NT), 0, s, pp,
-                           q);
+        if (lean)
+            hipLaunchKernelGGL((k_step_lean<G, R, DRIFT>), dim3((unsigned)grid), dim3(NT), 0, s,
+                               pm, q, tiles);
+        else
+            hipLaunchKernelGGL((k_step_paced<G, R, DRIFT>), dim3((unsigned)tiles), dim3(NT), 0, s,
+                               pm, q);
     } else {
         hipLaunchKernelGGL((k_step_fused<G, R, DRIFT>), dim3((unsigned)tiles), dim3(NT), 0, s, pp);
     }

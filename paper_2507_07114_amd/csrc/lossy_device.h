@@ -398,6 +398,7 @@ struct Chunk {
     int64_t c0;   // first element of the chunk
     int cv;       // valid elements of the chunk (0 .. NT * 8)
     int64_t e0;   // first element of this thread
+    int lane;     // e0 - c0
     int nv;       // valid elements of this thread (0..8)
     bool whole;   // wave-uniform: every thread owns 0 or 8 elements, 16-byte aligned
 };
@@ -416,11 +417,69 @@ __device__ __forceinline__ Chunk chunk_at(int64_t b, int64_t d, int64_t L, int c
     ch.c0 = pk0 + (int64_t)ch.c * (NT * kElems);
     const int64_t cv = pend - ch.c0;
     ch.cv = cv <= 0 ? 0 : (cv >= NT * kElems ? NT * kElems : (int)cv);
-    ch.e0 = ch.c0 + (int64_t)threadIdx.x * kElems;
+    ch.lane = (int)threadIdx.x * kElems;
+    ch.e0 = ch.c0 + ch.lane;
     const int64_t rem = pend - ch.e0;
     ch.nv = rem <= 0 ? 0 : (rem >= 8 ? 8 : (int)rem);
     ch.whole = (ch.c0 % 8 == 0) && ((pend - ch.c0) % 8 == 0 || pend >= ch.c0 + NT * kElems);
     return ch;
+}
+
+// Accesses of a thread's 8 elements of the chunk of a contiguous array or
+// row (`base` points at its element 0).  Whole tiles (W) go through a buffer
+// resource holding the chunk's valid bytes: its base is the same for every
+// lane, each lane adds a 32-bit offset, and lanes past the data read zeros
+// and write nothing.  Other tiles take the element-by-element form.
+template <class T>
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t chunk_rsrc(const T* base, const Chunk& ch) {
+    return row_rsrc(base + ch.c0, ch.cv * (int)sizeof(T));
+}
+
+template <bool W>
+__device__ __forceinline__ void load_chunk(const float* base, const Chunk& ch, Raw8<F32>& r) {
+    if (W) load_buf(chunk_rsrc(base, ch), ch.lane * 4, r);
+    else load_raw<false>(base + ch.e0, ch.nv, r);
+}
+
+// Plain (temporal) stores: master and moments are read again next step.
+template <bool W>
+__device__ __forceinline__ void store_chunk(float* base, const Chunk& ch, const float (&x)[8]) {
+    if (W) {
+        const __amdgpu_buffer_rsrc_t r = chunk_rsrc(base, ch);
+        const u32x4 a = {__float_as_uint(x[0]), __float_as_uint(x[1]), __float_as_uint(x[2]),
+                         __float_as_uint(x[3])};
+        const u32x4 b = {__float_as_uint(x[4]), __float_as_uint(x[5]), __float_as_uint(x[6]),
+                         __float_as_uint(x[7])};
+        __builtin_amdgcn_raw_buffer_store_b128(a, r, ch.lane * 4, 0, 0);
+        __builtin_amdgcn_raw_buffer_store_b128(b, r, ch.lane * 4 + 16, 0, 0);
+    } else {
+        store_f32x8<false>(base + ch.e0, ch.nv, x);
+    }
+}
+
+// Cache-policy bit of a non-temporal buffer store (gfx940-family `nt`).
+constexpr int kBufferNonTemporal = 2;
+
+// Replica rows: non-temporal stores of the rounded values.
+template <bool W>
+__device__ __forceinline__ void store_chunk(float* row, const Chunk& ch, const Packed8<F32>& x) {
+    if (W) {
+        const __amdgpu_buffer_rsrc_t r = chunk_rsrc(row, ch);
+        __builtin_amdgcn_raw_buffer_store_b128(x.r.a, r, ch.lane * 4, 0, kBufferNonTemporal);
+        __builtin_amdgcn_raw_buffer_store_b128(x.r.b, r, ch.lane * 4 + 16, 0, kBufferNonTemporal);
+    } else {
+        x.template store<false>(row + ch.e0, ch.nv);
+    }
+}
+
+template <bool W>
+__device__ __forceinline__ void store_chunk(uint16_t* row, const Chunk& ch,
+                                            const Packed8<BF16>& x) {
+    if (W)
+        __builtin_amdgcn_raw_buffer_store_b128(x.r.a, chunk_rsrc(row, ch), ch.lane * 2, 0,
+                                               kBufferNonTemporal);
+    else
+        x.template store<false>(row + ch.e0, ch.nv);
 }
 
 // ---------------------------------------------------------------------------

@@ -5,7 +5,8 @@
   is memory for them) is bit-identical to the unpaced step: every output,
   mask, count and drift figure, for both row types, with and without drift,
   mask outputs or a workspace, under schedules that are kept and schedules
-  laid out far too fast to keep.
+  laid out far too fast to keep, with a workgroup per tile or one round of
+  workgroups looping over the rounds.
 * Packets whose length is not a multiple of 8 elements, and fp32 rows whose
   stride is 4 (mod 8) elements, take the element-by-element access form;
   they match the oracle and the stage-by-stage chain.
@@ -58,6 +59,11 @@ SCHEDULES = [
     dict(overlap=1, resident=1, bytes_per_s=6.25e12),  # the default: one round at a time
     dict(overlap=2, resident=2, bytes_per_s=6.0e12),   # two rounds streaming at once
     dict(overlap=2, resident=3, bytes_per_s=5.0e14),   # far too fast to keep
+    # one round of workgroups looping over the rounds (steps in the plain
+    # configuration with whole tiles; the others fall back to a tile per
+    # workgroup), kept and far too fast to keep
+    dict(overlap=1, resident=1, bytes_per_s=6.25e12, persistent=1),
+    dict(overlap=1, resident=1, bytes_per_s=5.0e14, persistent=1),
 ]
 
 
