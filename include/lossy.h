@@ -353,9 +353,9 @@ LL_API int lossy_step_fused_noalloc(int32_t n, int64_t d, int64_t packet, uint64
  * is not kept and the speed falls back towards the unpaced one; too slow, the
  * step runs at the set rate.
  *   mode         LL_PACE_AUTO (default): paced where it was measured to pay,
- *                steps with bf16 gradient and replica rows, at least 32
- *                workers and at least 8 rounds (fp32 rows and few workers
- *                break even or lose); LL_PACE_ALWAYS; LL_PACE_NEVER.
+ *                steps with at least 32 workers and at least 8 rounds (few
+ *                workers break even or lose); LL_PACE_ALWAYS; LL_PACE_NEVER.
+ *                A round is at most 1024 tiles (4 MiB of a row per slot).
  *   bytes_per_s  rate the slots are laid out for (default 6.25e12).
  *   gap_us       time between the last gradient slot and the first replica
  *                slot, besides the master and moment writes (default 2).

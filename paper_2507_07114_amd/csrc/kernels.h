@@ -151,14 +151,15 @@ struct PaceParams {
     uint64_t guard;                // longest wait, ticks
 };
 
-// Pacing modes and defaults: auto paces steps of bf16 rows, at least
-// kPaceMinRows of them, spanning at least kPaceMinRounds
-// rounds; the schedule is laid out for kDefaultPaceRate bytes/s with
+// Pacing modes and defaults: auto paces steps of at least kPaceMinRows rows
+// spanning at least kPaceMinRounds rounds of at most kPaceMaxRoundTiles
+// tiles; the schedule is laid out for kDefaultPaceRate bytes/s with
 // kDefaultPaceGapUs between the gradient and replica sweeps, and starts
 // kPaceMarginUs after the anchor is written.
 enum { kPaceAuto = 0, kPaceAlways = 1, kPaceNever = 2 };
 constexpr int64_t kPaceMinRounds = 8;
 constexpr int kPaceMinRows = 32;
+constexpr int64_t kPaceMaxRoundTiles = 1024;
 constexpr double kDefaultPaceRate = 6.25e12;
 constexpr double kDefaultPaceGapUs = 2.0;
 constexpr double kDefaultPaceLeadUs = 4.0;

@@ -1057,15 +1057,16 @@ static bool pace_plan(const PaceSetting& st, bool lean, const FusedParams& p, co
                             : resident_per_cu(dev, k_step_paced<G, R, DRIFT>, NT, occupancy);
     const int k = st.overlap < 1 ? 1 : (st.overlap > 2 ? 2 : st.overlap);
     const int res = st.resident < k ? k : st.resident;
-    const int64_t gmax = (int64_t)(st.headroom * per_cu * cus / res);
+    // A round is at most kPaceMaxRoundTiles tiles (a row slot streams 4 MiB):
+    // rounds of every resident place of the fp32-row kernels (2048 tiles)
+    // were measured slower than rounds of half of them.
+    int64_t gmax = (int64_t)(st.headroom * per_cu * cus / res);
+    if (gmax > kPaceMaxRoundTiles) gmax = kPaceMaxRoundTiles;
     if (gmax < 1) return false;
     const int64_t rounds = (tiles + gmax - 1) / gmax;
-    // Auto: only where pacing was measured to pay, many bf16 rows (the N = 64
-    // step gains about 10%); fp32 rows and a few rows break even or lose.
-    if (st.mode == kPaceAuto &&
-        (rounds < kPaceMinRounds || p.n < kPaceMinRows || sizeof(typename G::T) != 2 ||
-         sizeof(typename R::T) != 2))
-        return false;
+    // Auto: only where pacing was measured to pay, many rows (the N = 64
+    // steps gain 5-10%); a few rows break even or lose.
+    if (st.mode == kPaceAuto && (rounds < kPaceMinRounds || p.n < kPaceMinRows)) return false;
     const int64_t g = (tiles + rounds - 1) / rounds;
     const double row_g = (double)NT * kElems * sizeof(typename G::T);
     const double row_r = (double)NT * kElems * sizeof(typename R::T);
