@@ -449,6 +449,10 @@ def main():
         "hbm_copy_probe_gbs": round(copy_gbs, 1),
         "hbm_probes_gbs": probes,
         "frac_of_best_copy_probe": round(value / probes["copy_16B"], 4),
+        # per-step event times: a paced step either keeps its schedule (the
+        # minimum) or slips; `value` is over all of them
+        "step_ms": {"min": round(min(ms), 4), "median": round(float(np.median(ms)), 4),
+                    "max": round(max(ms), 4)},
         "roofline": {
             "bound": "hbm",
             "kernel": ("stage chain: masks x2, k_aggregate, k_shard_step, k_broadcast, k_drift "
