@@ -356,7 +356,8 @@ LL_API int lossy_step_fused_noalloc(int32_t n, int64_t d, int64_t packet, uint64
  *                steps with at least 32 workers and at least 8 rounds (few
  *                workers break even or lose); LL_PACE_ALWAYS; LL_PACE_NEVER.
  *                A round is at most 1024 tiles (4 MiB of a row per slot).
- *   bytes_per_s  rate the slots are laid out for (default 6.25e12).
+ *   bytes_per_s  rate the slots are laid out for (default 6.25e12), for
+ *                steps whose replica rows are bf16.
  *   gap_us       time between the last gradient slot and the first replica
  *                slot, besides the master and moment writes (default 2).
  *   lead_us      time from a round's start to its first gradient slot,
@@ -384,6 +385,10 @@ LL_API int lossy_step_fused_noalloc(int32_t n, int64_t d, int64_t packet, uint64
  *                worth of workgroups that loop over the rounds, so no
  *                workgroup starts or leaves between rounds; needs overlap
  *                and resident 1.  0: one workgroup per tile (default 0).
+ *   bytes_per_s_f32  the same for steps whose replica rows are fp32 (their
+ *                workgroups are 128 threads with two loads per row each;
+ *                measured to keep their schedule at a lower rate; default
+ *                5.9e12).
  * A workgroup that starts behind its round (its place freed late) issues the
  * rows whose slots have passed at once and then keeps the round's slots.
  * The setting is process-wide and read at each call.  A paced step enqueues,
@@ -395,8 +400,9 @@ LL_API int lossy_step_fused_noalloc(int32_t n, int64_t d, int64_t packet, uint64
  * device variable.  Overlapping paced steps on one device can read each
  * other's start time, which costs speed but changes no result.
  * ll_set_pacing returns LL_EINVAL for an unknown mode or a field outside the
- * ranges above (bytes_per_s in (0, 1e15), gap_us, lead_us and tail_us in
- * [0, 1e4], persistent 0 or 1 and only with overlap and resident 1);
+ * ranges above (bytes_per_s and bytes_per_s_f32 in (0, 1e15), gap_us,
+ * lead_us and tail_us in [0, 1e4], persistent 0 or 1 and only with overlap
+ * and resident 1);
  * ll_get_pacing fills `out` (host).
  */
 enum { LL_PACE_AUTO = 0, LL_PACE_ALWAYS = 1, LL_PACE_NEVER = 2 };
@@ -410,6 +416,7 @@ typedef struct {
     double headroom;
     double tail_us;
     int32_t persistent;
+    double bytes_per_s_f32;
 } ll_pacing;
 
 LL_API int ll_set_pacing(const ll_pacing* cfg);

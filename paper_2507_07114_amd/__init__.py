@@ -234,7 +234,7 @@ class Pacing(ctypes.Structure):
                 ("gap_us", ctypes.c_double), ("lead_us", ctypes.c_double),
                 ("overlap", ctypes.c_int32), ("resident", ctypes.c_int32),
                 ("headroom", ctypes.c_double), ("tail_us", ctypes.c_double),
-                ("persistent", ctypes.c_int32)]
+                ("persistent", ctypes.c_int32), ("bytes_per_s_f32", ctypes.c_double)]
 
 
 PACE_MODES = {"auto": 0, "always": 1, "never": 2}
@@ -242,13 +242,14 @@ PACE_MODES = {"auto": 0, "always": 1, "never": 2}
 
 def ll_set_pacing(mode: str = "auto", bytes_per_s: float = 6.25e12, gap_us: float = 2.0,
                   lead_us: float = 4.0, overlap: int = 1, resident: int = 1,
-                  headroom: float = 1.0, tail_us: float = 3.0, persistent: int = 0) -> None:
+                  headroom: float = 1.0, tail_us: float = 3.0, persistent: int = 0,
+                  bytes_per_s_f32: float = 5.9e12) -> None:
     """Process-wide pacing of lossy_step_fused (a performance setting; see
     include/lossy.h)."""
     if mode not in PACE_MODES:
         raise ValueError(f"unknown pacing mode {mode!r}")
     cfg = Pacing(PACE_MODES[mode], bytes_per_s, gap_us, lead_us, overlap, resident, headroom,
-                 tail_us, persistent)
+                 tail_us, persistent, bytes_per_s_f32)
     _check("ll_set_pacing", _load().ll_set_pacing(ctypes.byref(cfg)))
 
 
@@ -258,7 +259,8 @@ def ll_get_pacing() -> dict:
     mode = {v: k for k, v in PACE_MODES.items()}[cfg.mode]
     return dict(mode=mode, bytes_per_s=cfg.bytes_per_s, gap_us=cfg.gap_us, lead_us=cfg.lead_us,
                 overlap=cfg.overlap, resident=cfg.resident, headroom=cfg.headroom,
-                tail_us=cfg.tail_us, persistent=cfg.persistent)
+                tail_us=cfg.tail_us, persistent=cfg.persistent,
+                bytes_per_s_f32=cfg.bytes_per_s_f32)
 
 
 def ll_last_error() -> str:

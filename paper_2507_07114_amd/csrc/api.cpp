@@ -334,6 +334,8 @@ int ll_set_pacing(const ll_pacing* cfg) {
         return fail(LL_EINVAL, "unknown pacing mode %d", cfg->mode);
     if (!(cfg->bytes_per_s > 0.0 && cfg->bytes_per_s < 1e15))
         return fail(LL_EINVAL, "bytes_per_s must lie in (0, 1e15)");
+    if (!(cfg->bytes_per_s_f32 > 0.0 && cfg->bytes_per_s_f32 < 1e15))
+        return fail(LL_EINVAL, "bytes_per_s_f32 must lie in (0, 1e15)");
     if (!(cfg->gap_us >= 0.0 && cfg->gap_us <= 1e4))
         return fail(LL_EINVAL, "gap_us must lie in [0, 1e4]");
     if (!(cfg->lead_us >= 0.0 && cfg->lead_us <= 1e4))
@@ -352,7 +354,7 @@ int ll_set_pacing(const ll_pacing* cfg) {
         return fail(LL_EINVAL, "persistent pacing needs overlap=1 and resident=1");
     set_pace_setting(PaceSetting{cfg->mode, cfg->bytes_per_s, cfg->gap_us, cfg->lead_us,
                                  cfg->overlap, cfg->resident, cfg->headroom, cfg->tail_us,
-                                 cfg->persistent});
+                                 cfg->persistent, cfg->bytes_per_s_f32});
     return ok();
 }
 
@@ -368,6 +370,7 @@ int ll_get_pacing(ll_pacing* out) {
     out->headroom = st.headroom;
     out->tail_us = st.tail_us;
     out->persistent = st.persistent;
+    out->bytes_per_s_f32 = st.bytes_per_s_f32;
     return ok();
 }
 

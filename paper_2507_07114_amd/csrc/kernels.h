@@ -153,7 +153,8 @@ struct PaceParams {
 
 // Pacing modes and defaults: auto paces steps of at least kPaceMinRows rows
 // spanning at least kPaceMinRounds rounds of at most kPaceMaxRoundTiles
-// tiles; the schedule is laid out for kDefaultPaceRate bytes/s with
+// tiles; the schedule is laid out for kDefaultPaceRate bytes/s
+// (kDefaultPaceRateF32 for steps with fp32 replica rows) with
 // kDefaultPaceGapUs between the gradient and replica sweeps, and starts
 // kPaceMarginUs after the anchor is written.
 enum { kPaceAuto = 0, kPaceAlways = 1, kPaceNever = 2 };
@@ -161,6 +162,7 @@ constexpr int64_t kPaceMinRounds = 8;
 constexpr int kPaceMinRows = 32;
 constexpr int64_t kPaceMaxRoundTiles = 1024;
 constexpr double kDefaultPaceRate = 6.25e12;
+constexpr double kDefaultPaceRateF32 = 5.9e12;
 constexpr double kDefaultPaceGapUs = 2.0;
 constexpr double kDefaultPaceLeadUs = 4.0;
 constexpr int kDefaultPaceOverlap = 1;
@@ -182,6 +184,7 @@ struct PaceSetting {
     double headroom;     // fraction of the resident places the rounds may fill
     double tail_us;      // allowance after a round's last slot
     int persistent;      // 1: one round of workgroups loops over the rounds (plain steps)
+    double bytes_per_s_f32;  // rate for steps whose replica rows are fp32
 };
 PaceSetting get_pace_setting();
 void set_pace_setting(const PaceSetting& s);

@@ -970,6 +970,7 @@ std::atomic<int> g_pace_resident{kDefaultPaceResident};
 std::atomic<double> g_pace_headroom{kDefaultPaceHeadroom};
 std::atomic<double> g_pace_tail_us{kDefaultPaceTailUs};
 std::atomic<int> g_pace_persistent{kDefaultPacePersistent};
+std::atomic<double> g_pace_rate_f32{kDefaultPaceRateF32};
 
 // Compute units and clock rate of a device, and resident workgroups per
 // compute unit of a kernel, looked up once per device into fixed tables (no
@@ -1017,7 +1018,8 @@ int resident_per_cu(int dev, K kernel, int threads, int (&table)[kMaxDevices]) {
 PaceSetting get_pace_setting() {
     return PaceSetting{g_pace_mode.load(), g_pace_rate.load(), g_pace_gap_us.load(),
                        g_pace_lead_us.load(), g_pace_overlap.load(), g_pace_resident.load(),
-                       g_pace_headroom.load(), g_pace_tail_us.load(), g_pace_persistent.load()};
+                       g_pace_headroom.load(), g_pace_tail_us.load(), g_pace_persistent.load(),
+                       g_pace_rate_f32.load()};
 }
 
 void set_pace_setting(const PaceSetting& st) {
@@ -1030,6 +1032,7 @@ void set_pace_setting(const PaceSetting& st) {
     g_pace_headroom.store(st.headroom);
     g_pace_tail_us.store(st.tail_us);
     g_pace_persistent.store(st.persistent);
+    g_pace_rate_f32.store(st.bytes_per_s_f32);
 }
 
 // Lay out the schedule of a paced step with `tiles` tiles, or return false
@@ -1048,7 +1051,10 @@ template <class G, class R, bool DRIFT>
 static bool pace_plan(const PaceSetting& st, bool lean, const FusedParams& p, const PaceHint& h,
                       int64_t tiles, PaceParams* q, int64_t* grid, uint64_t* margin) {
     constexpr int NT = R::kPacketThreads;
-    if (st.mode == kPaceNever || !(st.bytes_per_s > 0.0) || tiles <= 0) return false;
+    // Steps with fp32 replica rows (128-thread workgroups, two loads per row
+    // and thread) keep their schedule at a lower rate than bf16 rows.
+    const double rate = sizeof(typename R::T) == 4 ? st.bytes_per_s_f32 : st.bytes_per_s;
+    if (st.mode == kPaceNever || !(rate > 0.0) || tiles <= 0) return false;
     int dev = 0, cus = 0;
     double tick_hz = 0.0;
     if (hipGetDevice(&dev) != hipSuccess || !device_info(dev, &cus, &tick_hz)) return false;
@@ -1071,7 +1077,7 @@ static bool pace_plan(const PaceSetting& st, bool lean, const FusedParams& p, co
     const double row_g = (double)NT * kElems * sizeof(typename G::T);
     const double row_r = (double)NT * kElems * sizeof(typename R::T);
     const double state = (double)NT * kElems * 4.0 * (p.opt.kind + 1);
-    const double fp = 256.0 * tick_hz * k / st.bytes_per_s;  // 1/256 ticks per byte of a round
+    const double fp = 256.0 * tick_hz * k / rate;  // 1/256 ticks per byte of a round
     const double us = 1e-6 * tick_hz * 256.0;                 // 1/256 ticks per microsecond
     const double qg = h.q_g < 0.0 ? 0.0 : (h.q_g > 1.0 ? 1.0 : h.q_g);
     const double qb = h.q_b < 0.0 ? 0.0 : (h.q_b > 1.0 ? 1.0 : h.q_b);

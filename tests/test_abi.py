@@ -242,7 +242,8 @@ def test_pacing_setting_round_trips_and_rejects_bad_values():
     before = ll.ll_get_pacing()
     try:
         want = dict(mode="never", bytes_per_s=5.0e12, gap_us=1.5, lead_us=3.0, overlap=1,
-                    resident=2, headroom=0.75, tail_us=1.25, persistent=0)
+                    resident=2, headroom=0.75, tail_us=1.25, persistent=0,
+                    bytes_per_s_f32=4.5e12)
         ll.ll_set_pacing(**want)
         assert ll.ll_get_pacing() == want
         for bad in ((0.0, 1.0, 1.0, 2, 3), (-1.0, 1.0, 1.0, 2, 3), (2e15, 1.0, 1.0, 2, 3),
@@ -251,13 +252,15 @@ def test_pacing_setting_round_trips_and_rejects_bad_values():
                     (6e12, 1.0, 1.0, 1, 5), (6e12, 1.0, 1.0, 1, 1, 0.0), (6e12, 1.0, 1.0, 1, 1, 1.5),
                     (6e12, 1.0, 1.0, 1, 1, 1.0, -1.0), (6e12, 1.0, 1.0, 1, 1, 1.0, 2e4),
                     (6e12, 1.0, 1.0, 1, 1, 1.0, 1.0, 2), (6e12, 1.0, 1.0, 1, 1, 1.0, 1.0, -1),
-                    (6e12, 1.0, 1.0, 2, 2, 1.0, 1.0, 1), (6e12, 1.0, 1.0, 1, 2, 1.0, 1.0, 1)):
+                    (6e12, 1.0, 1.0, 2, 2, 1.0, 1.0, 1), (6e12, 1.0, 1.0, 1, 2, 1.0, 1.0, 1),
+                    (6e12, 1.0, 1.0, 1, 1, 1.0, 1.0, 0, 0.0),
+                    (6e12, 1.0, 1.0, 1, 1, 1.0, 1.0, 0, 2e15)):
             with pytest.raises(ll.LossyError):
                 ll.ll_set_pacing("auto", *bad)
         lib = _raw()
         lib.ll_set_pacing.argtypes = [ctypes.c_void_p]
         lib.ll_last_error.restype = ctypes.c_char_p
-        cfg = ll.Pacing(7, 6e12, 2.0, 2.5, 2, 2, 0.9, 2.5, 0)
+        cfg = ll.Pacing(7, 6e12, 2.0, 2.5, 2, 2, 0.9, 2.5, 0, 6e12)
         assert lib.ll_set_pacing(ctypes.byref(cfg)) == -1
         assert "unknown pacing mode 7" in lib.ll_last_error().decode()
         assert lib.ll_set_pacing(None) == -1

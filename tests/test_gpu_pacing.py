@@ -84,7 +84,9 @@ def test_paced_step_is_bit_identical_to_unpaced(name, sched, masks_out, drift, w
     for t in range(2):
         wl.draw_grads(w, t, device=DEV, ld=a.ld, out=a.grads)
         b.grads.copy_(a.grads)
-        ll.ll_set_pacing("always", gap_us=2.0, lead_us=4.0, headroom=0.9, **cfg)
+        # the schedule's rate for either row type
+        ll.ll_set_pacing("always", gap_us=2.0, lead_us=4.0, headroom=0.9,
+                         bytes_per_s_f32=cfg["bytes_per_s"], **cfg)
         _step(a, t, masks_out=masks_out, drift=drift, workspace=workspace)
         ll.ll_set_pacing("never")
         _step(b, t, masks_out=masks_out, drift=drift, workspace=workspace)
