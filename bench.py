@@ -228,7 +228,7 @@ def cpu_baseline(w, dev, packets_sample: int):
     b = algorithmic_bytes(w, mg, mb, lens, True)["total"]
     return dict(value=round(b / wall / 1e9, 4), unit="GB/s",
                 cores=max(1, int(round(cpu / wall))), kind="oracle",
-                sample=f"{len(sample)} of {P} packets (every {max(1, P // packets_sample)}th), "
+                sample=f"{len(sample)} of {P} packets (one in every {max(1, P // packets_sample)}), "
                        f"one step incl. masks and drift, {wall:.1f} s wall; "
                        f"{len(os.sched_getaffinity(0))} host cores available ({cpu_model()})")
 
