@@ -355,7 +355,9 @@ LL_API int lossy_step_fused_noalloc(int32_t n, int64_t d, int64_t packet, uint64
  *   mode         LL_PACE_AUTO (default): paced where it was measured to pay,
  *                steps with at least 32 workers and at least 8 rounds (few
  *                workers break even or lose); LL_PACE_ALWAYS; LL_PACE_NEVER.
- *                A round is at most 1024 tiles (4 MiB of a row per slot).
+ *                A round takes every resident workgroup place (bf16
+ *                rows) or at most 1024 tiles (fp32 rows, 4 MiB of a row
+ *                per slot).
  *   bytes_per_s  rate the slots are laid out for (default 6.25e12), for
  *                steps whose replica rows are bf16.
  *   gap_us       time between the last gradient slot and the first replica

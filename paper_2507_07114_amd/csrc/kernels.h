@@ -152,8 +152,8 @@ struct PaceParams {
 };
 
 // Pacing modes and defaults: auto paces steps of at least kPaceMinRows rows
-// spanning at least kPaceMinRounds rounds of at most kPaceMaxRoundTiles
-// tiles; the schedule is laid out for kDefaultPaceRate bytes/s
+// spanning at least kPaceMinRounds rounds (of at most kPaceMaxRoundTiles
+// tiles for fp32 rows); the schedule is laid out for kDefaultPaceRate bytes/s
 // (kDefaultPaceRateF32 for steps with fp32 replica rows) with
 // kDefaultPaceGapUs between the gradient and replica sweeps, and starts
 // kPaceMarginUs after the anchor is written.

@@ -1063,11 +1063,14 @@ static bool pace_plan(const PaceSetting& st, bool lean, const FusedParams& p, co
                             : resident_per_cu(dev, k_step_paced<G, R, DRIFT>, NT, occupancy);
     const int k = st.overlap < 1 ? 1 : (st.overlap > 2 ? 2 : st.overlap);
     const int res = st.resident < k ? k : st.resident;
-    // A round is at most kPaceMaxRoundTiles tiles (a row slot streams 4 MiB):
-    // rounds of every resident place of the fp32-row kernels (2048 tiles)
-    // were measured slower than rounds of half of them.
+    // A round of an fp32-row kernel is at most kPaceMaxRoundTiles tiles (a
+    // row slot streams 4 MiB): rounds of every resident place of those
+    // kernels (2048 tiles) were measured slower than rounds of half of them.
+    // Rounds of the bf16-row kernels take every place (1008 tiles with
+    // drift, 1536 without): capped at 1024, the 1536-place kernel's next
+    // round starts early in the spare places and the schedule is not kept.
     int64_t gmax = (int64_t)(st.headroom * per_cu * cus / res);
-    if (gmax > kPaceMaxRoundTiles) gmax = kPaceMaxRoundTiles;
+    if (sizeof(typename R::T) == 4 && gmax > kPaceMaxRoundTiles) gmax = kPaceMaxRoundTiles;
     if (gmax < 1) return false;
     const int64_t rounds = (tiles + gmax - 1) / gmax;
     // Auto: only where pacing was measured to pay, many rows (the N = 64
