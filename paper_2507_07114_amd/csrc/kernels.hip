@@ -333,7 +333,7 @@ __device__ __forceinline__ void drift_chunk(const DriftParams& p, const Chunk& c
     } else {
         load8<R, W>(reps + ch.e0, ch.nv, r);
     }
-    Drift8 acc;
+    Drift8<R> acc;
     acc.init(false, r);
     for (int i0 = 0; i0 < p.n; i0 += kBatchDrift) {
         Raw8<R> raw[kBatchDrift];
@@ -572,7 +572,7 @@ __device__ __forceinline__ void step_chunk(const FusedParams& p, const Chunk& ch
     }
     if (!DRIFT) return;
     // Stale rows (broadcast lost) in ascending order, after every store.
-    Drift8 acc;
+    Drift8<R> acc;
     float rv[8];
 #pragma unroll
     for (int j = 0; j < 8; ++j) rv[j] = r.value(j);
@@ -779,7 +779,7 @@ __device__ __forceinline__ void lean_tile(const FusedParams& p, int64_t tile, Cl
             store_chunk<true>(reps + (int64_t)i * p.ld_r, ch, r);
         }
         if (DRIFT) {
-            Drift8 acc;
+            Drift8<R> acc;
             float rv[8];
 #pragma unroll
             for (int j = 0; j < 8; ++j) rv[j] = r.value(j);
@@ -1066,9 +1066,9 @@ static bool pace_plan(const PaceSetting& st, bool lean, const FusedParams& p, co
     // A round of an fp32-row kernel is at most kPaceMaxRoundTiles tiles (a
     // row slot streams 4 MiB): rounds of every resident place of those
     // kernels (2048 tiles) were measured slower than rounds of half of them.
-    // Rounds of the bf16-row kernels take every place (1008 tiles with
-    // drift, 1536 without): capped at 1024, the 1536-place kernel's next
-    // round starts early in the spare places and the schedule is not kept.
+    // Rounds of the bf16-row kernels take every place (1280 with drift,
+    // 1536 without): capped at 1024, the next round's workgroups start early
+    // in the spare places and the schedule is not kept.
     int64_t gmax = (int64_t)(st.headroom * per_cu * cus / res);
     if (sizeof(typename R::T) == 4 && gmax > kPaceMaxRoundTiles) gmax = kPaceMaxRoundTiles;
     if (gmax < 1) return false;

@@ -791,9 +791,47 @@ __device__ __forceinline__ void update8(const OptParams& o, float (&th)[8], floa
 // Drift accumulation for the 8 elements of one thread.  Values are compared
 // with the reference r = c(theta) of the element: d = x - r in fp64.
 // ---------------------------------------------------------------------------
+// Range bounds of one thread's 8 elements: the largest and smallest value
+// seen per element.  Values of bf16 rows are kept as bf16 bit patterns, two
+// to a register (they are bf16 values, so nothing is rounded).
+template <class R>
+struct Bounds8 {
+    float hi[8], lo[8];
+    __device__ __forceinline__ void init(int j, float h, float l) { hi[j] = h; lo[j] = l; }
+    __device__ __forceinline__ void add(int j, float x) {
+        hi[j] = fmaxf(hi[j], x);
+        lo[j] = fminf(lo[j], x);
+    }
+    __device__ __forceinline__ float high(int j) const { return hi[j]; }
+    __device__ __forceinline__ float low(int j) const { return lo[j]; }
+};
+
+template <>
+struct Bounds8<BF16> {
+    uint32_t hi[4], lo[4];
+    __device__ __forceinline__ static float get(const uint32_t (&w)[4], int j) {
+        return __uint_as_float((j & 1) ? (w[j >> 1] & 0xFFFF0000u) : (w[j >> 1] << 16));
+    }
+    __device__ __forceinline__ static void put(uint32_t (&w)[4], int j, float v) {
+        const uint32_t b = __float_as_uint(v) >> 16;
+        w[j >> 1] = (j & 1) ? ((w[j >> 1] & 0xFFFFu) | (b << 16)) : ((w[j >> 1] & 0xFFFF0000u) | b);
+    }
+    __device__ __forceinline__ void init(int j, float h, float l) {
+        put(hi, j, h);
+        put(lo, j, l);
+    }
+    __device__ __forceinline__ void add(int j, float x) {
+        put(hi, j, fmaxf(get(hi, j), x));
+        put(lo, j, fminf(get(lo, j), x));
+    }
+    __device__ __forceinline__ float high(int j) const { return get(hi, j); }
+    __device__ __forceinline__ float low(int j) const { return get(lo, j); }
+};
+
+template <class R>
 struct Drift8 {
     double s1[8], s2[8];
-    float hi[8], lo[8];
+    Bounds8<R> b;
     double abs_sum;
 
     __device__ __forceinline__ void init(bool any_equal_ref, const float (&r)[8]) {
@@ -801,8 +839,8 @@ struct Drift8 {
         for (int j = 0; j < 8; ++j) {
             s1[j] = 0.0;
             s2[j] = 0.0;
-            hi[j] = any_equal_ref ? r[j] : -__builtin_inff();
-            lo[j] = any_equal_ref ? r[j] : __builtin_inff();
+            b.init(j, any_equal_ref ? r[j] : -__builtin_inff(),
+                   any_equal_ref ? r[j] : __builtin_inff());
         }
         abs_sum = 0.0;
     }
@@ -814,8 +852,7 @@ struct Drift8 {
                 s1[j] = s1[j] + d;
                 s2[j] = __fma_rn(d, d, s2[j]);
                 abs_sum = abs_sum + fabs(d);
-                hi[j] = fmaxf(hi[j], x[j]);
-                lo[j] = fminf(lo[j], x[j]);
+                b.add(j, x[j]);
             }
         }
     }
@@ -828,7 +865,7 @@ struct Drift8 {
             if (j < nv) {
                 const double ps = (double)n * s2[j] - s1[j] * s1[j];
                 pair = pair + (ps > 0.0 ? ps : 0.0);
-                const double rg = (double)hi[j] - (double)lo[j];
+                const double rg = (double)b.high(j) - (double)b.low(j);
                 range = rg > range ? rg : range;
             }
         }
