@@ -333,7 +333,7 @@ __device__ __forceinline__ void drift_chunk(const DriftParams& p, const Chunk& c
     } else {
         load8<R, W>(reps + ch.e0, ch.nv, r);
     }
-    Drift8<R> acc;
+    Drift8<FloatBounds8> acc;
     acc.init(false, r);
     for (int i0 = 0; i0 < p.n; i0 += kBatchDrift) {
         Raw8<R> raw[kBatchDrift];
@@ -572,7 +572,7 @@ __device__ __forceinline__ void step_chunk(const FusedParams& p, const Chunk& ch
     }
     if (!DRIFT) return;
     // Stale rows (broadcast lost) in ascending order, after every store.
-    Drift8<R> acc;
+    Drift8<typename StepBounds8<R>::type> acc;
     float rv[8];
 #pragma unroll
     for (int j = 0; j < 8; ++j) rv[j] = r.value(j);
@@ -779,7 +779,7 @@ __device__ __forceinline__ void lean_tile(const FusedParams& p, int64_t tile, Cl
             store_chunk<true>(reps + (int64_t)i * p.ld_r, ch, r);
         }
         if (DRIFT) {
-            Drift8<R> acc;
+            Drift8<typename StepBounds8<R>::type> acc;
             float rv[8];
 #pragma unroll
             for (int j = 0; j < 8; ++j) rv[j] = r.value(j);

@@ -792,12 +792,13 @@ __device__ __forceinline__ void update8(const OptParams& o, float (&th)[8], floa
 // with the reference r = c(theta) of the element: d = x - r in fp64.
 // ---------------------------------------------------------------------------
 // Range bounds of one thread's 8 elements: the largest and smallest value
-// seen per element.  Values of bf16 rows are kept as bf16 bit patterns, two
-// to a register (they are bf16 values, so nothing is rounded).
-template <class R>
-struct Bounds8 {
+// seen per element, as floats.
+struct FloatBounds8 {
     float hi[8], lo[8];
-    __device__ __forceinline__ void init(int j, float h, float l) { hi[j] = h; lo[j] = l; }
+    __device__ __forceinline__ void init(int j, float h, float l) {
+        hi[j] = h;
+        lo[j] = l;
+    }
     __device__ __forceinline__ void add(int j, float x) {
         hi[j] = fmaxf(hi[j], x);
         lo[j] = fminf(lo[j], x);
@@ -806,8 +807,13 @@ struct Bounds8 {
     __device__ __forceinline__ float low(int j) const { return lo[j]; }
 };
 
-template <>
-struct Bounds8<BF16> {
+// The same for values that are bf16 (rows of bf16 replicas): kept as bf16
+// bit patterns, two to a register, so nothing is rounded.  Half the
+// registers of FloatBounds8 for a few more ALU operations per value; the
+// fused step, whose occupancy is set by its registers and which reads only
+// the stale rows, takes this form; the standalone drift pass, which reads
+// every row, keeps FloatBounds8.
+struct Bf16Bounds8 {
     uint32_t hi[4], lo[4];
     __device__ __forceinline__ static float get(const uint32_t (&w)[4], int j) {
         return __uint_as_float((j & 1) ? (w[j >> 1] & 0xFFFF0000u) : (w[j >> 1] << 16));
@@ -829,9 +835,18 @@ struct Bounds8<BF16> {
 };
 
 template <class R>
+struct StepBounds8 {
+    using type = FloatBounds8;
+};
+template <>
+struct StepBounds8<BF16> {
+    using type = Bf16Bounds8;
+};
+
+template <class B>
 struct Drift8 {
     double s1[8], s2[8];
-    Bounds8<R> b;
+    B b;
     double abs_sum;
 
     __device__ __forceinline__ void init(bool any_equal_ref, const float (&r)[8]) {
