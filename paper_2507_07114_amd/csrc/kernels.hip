@@ -578,7 +578,7 @@ __device__ __forceinline__ void step_chunk(const FusedParams& p, const Chunk& ch
     for (int j = 0; j < 8; ++j) rv[j] = r.value(j);
     acc.init(RC > 0, rv);
     RowWalk stale(s_words[1], p.n, true, -1);
-    stream_rows<kDepthStale, R, W>(
+    stream_rows<RingDepth<Pace>::stale, R, W>(
         reps, p.ld_r, ch, stale, [&](int row) { pace.stale(row); },
         [&](const Raw8<R>& raw) {
             float x[8];
@@ -747,7 +747,7 @@ __device__ __forceinline__ void lean_tile(const FusedParams& p, int64_t tile, Cl
 #pragma unroll
         for (int j = 0; j < 8; ++j) g[j] = 0.0f;
         RowWalk walk(s_words[0], p.n, false, -1);
-        stream_rows<kDepthGrad, G, true>(
+        stream_rows<RingDepth<ClockPace>::grad, G, true>(
             reinterpret_cast<const typename G::T*>(p.grads), p.ld_g, ch, walk,
             [&](int row) { pace.grad(row); },
             [&](const Raw8<G>& raw) {
@@ -785,7 +785,7 @@ __device__ __forceinline__ void lean_tile(const FusedParams& p, int64_t tile, Cl
             for (int j = 0; j < 8; ++j) rv[j] = r.value(j);
             acc.init(RC > 0, rv);
             RowWalk stale(s_words[1], p.n, true, -1);
-            stream_rows<kDepthStale, R, true>(
+            stream_rows<RingDepth<ClockPace>::stale, R, true>(
                 reps, p.ld_r, ch, stale, [&](int row) { pace.stale(row); },
                 [&](const Raw8<R>& raw) {
                     float x[8];

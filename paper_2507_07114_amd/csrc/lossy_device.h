@@ -22,7 +22,9 @@ constexpr int kMaxWorkers = 1024;
 constexpr int kMaxWords = kMaxWorkers / 64;
 // Row loads in flight per thread while streaming the arrived gradient rows
 // and the stale replica rows (a ring: the load of row j + depth is issued as
-// soon as row j has been used).
+// soon as row j has been used) in an unpaced step, where a workgroup's own
+// loads are all that keeps the memory busy.  The paced step's depth is
+// RingDepth<ClockPace> below.
 constexpr int kDepthGrad = 4;
 constexpr int kDepthStale = 4;
 // Gradient rows per batch of the stale-fill estimator, which reads every row.
@@ -586,6 +588,23 @@ struct NoPace {
 // access of row i in the gradient, replica and stale-read sweeps waits for
 // base + off + i * delta of that sweep.  A slot further away than `guard`
 // ticks (a stale or foreign anchor) is not waited for, so every wait ends.
+struct ClockPace;
+
+// Rows in flight per thread of each sweep, by pacing.  Paced, the whole chip
+// streams each row at its slot, and two rows in flight keep the sweeps at the
+// schedule's rate while queueing half as much in the memory system as four:
+// with four, a memory stall left more workgroups late and far more steps
+// slipped (the 7B-shard step kept its schedule in 7-73% of steps with four,
+// 71-93% with two).
+template <class Pace>
+struct RingDepth {
+    static constexpr int grad = kDepthGrad, stale = kDepthStale;
+};
+template <>
+struct RingDepth<ClockPace> {
+    static constexpr int grad = 2, stale = 2;
+};
+
 struct ClockPace {
     uint64_t base;  // round start, ticks (set by begin())
     uint64_t off_g, off_r, off_s;  // sweep starts, 1/256 ticks after base
@@ -722,7 +741,7 @@ __device__ __forceinline__ void aggregate8(const typename E::T* grads, int64_t l
     const bool ht = var.kind == kEstHorvitzThompson;
     const int sure_row = (ht && !reliable_packet) ? var.owner : -1;
     RowWalk walk(gm, n, false, sure_row);
-    stream_rows<kDepthGrad, E, W>(
+    stream_rows<RingDepth<Pace>::grad, E, W>(
         grads, ld, ch, walk, [&](int row) { pace.grad(row); },
         [&](const Raw8<E>& raw) {
             float x[8];
