@@ -358,7 +358,7 @@ LL_API int lossy_step_fused_noalloc(int32_t n, int64_t d, int64_t packet, uint64
  *                A round takes every resident workgroup place (bf16
  *                rows) or at most 1024 tiles (fp32 rows, 4 MiB of a row
  *                per slot).
- *   bytes_per_s  rate the slots are laid out for (default 6.2e12), for
+ *   bytes_per_s  rate the slots are laid out for (default 6.3e12), for
  *                steps whose replica rows are bf16.
  *   gap_us       time between the last gradient slot and the first replica
  *                slot, besides the master and moment writes (default 2).

@@ -240,7 +240,7 @@ class Pacing(ctypes.Structure):
 PACE_MODES = {"auto": 0, "always": 1, "never": 2}
 
 
-def ll_set_pacing(mode: str = "auto", bytes_per_s: float = 6.2e12, gap_us: float = 2.0,
+def ll_set_pacing(mode: str = "auto", bytes_per_s: float = 6.3e12, gap_us: float = 2.0,
                   lead_us: float = 4.0, overlap: int = 1, resident: int = 1,
                   headroom: float = 1.0, tail_us: float = 3.0, persistent: int = 0,
                   bytes_per_s_f32: float = 5.9e12) -> None:

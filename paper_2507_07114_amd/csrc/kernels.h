@@ -161,7 +161,7 @@ enum { kPaceAuto = 0, kPaceAlways = 1, kPaceNever = 2 };
 constexpr int64_t kPaceMinRounds = 8;
 constexpr int kPaceMinRows = 32;
 constexpr int64_t kPaceMaxRoundTiles = 1024;
-constexpr double kDefaultPaceRate = 6.2e12;
+constexpr double kDefaultPaceRate = 6.3e12;
 constexpr double kDefaultPaceRateF32 = 5.9e12;
 constexpr double kDefaultPaceGapUs = 2.0;
 constexpr double kDefaultPaceLeadUs = 4.0;
