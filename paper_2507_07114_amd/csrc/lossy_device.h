@@ -594,8 +594,8 @@ struct ClockPace;
 // streams each row at its slot, and two rows in flight keep the sweeps at the
 // schedule's rate while queueing half as much in the memory system as four:
 // with four, a memory stall left more workgroups late and far more steps
-// slipped (the 7B-shard step kept its schedule in 7-73% of steps with four,
-// 71-93% with two).
+// slipped (the 7B-shard step kept its schedule in 7-71% of steps with four,
+// 71-97% with two, on the same three boxes).
 template <class Pace>
 struct RingDepth {
     static constexpr int grad = kDepthGrad, stale = kDepthStale;
