@@ -48,11 +48,14 @@ def _step(dev: parity.DeviceState, t: int, *, masks_out: bool, drift: bool, work
 
 PACED = {
     # workloads scaled so that the step spans several rounds of resident
-    # workgroups at the default layout, with ragged tails
-    "n64_llama7b_shard_bf16_adam": dict(d=4096 * 2100 + 3280),
-    "n64_d48m_f32_sgd_drift": dict(d=2048 * 4000 + 1000),
-    "n8_d16m_bf16_adam": dict(d=2048 * 9000 + 77),
-    "n16_d256m_f32_ge_momentum": dict(d=4096 * 3000 + 2056),
+    # workgroups at the default layout, with ragged tails; the last two have
+    # several mask words per packet, the last one ragged
+    "n64_llama7b_shard_bf16_adam": ("n64_llama7b_shard_bf16_adam", dict(d=4096 * 2100 + 3280)),
+    "n64_d48m_f32_sgd_drift": ("n64_d48m_f32_sgd_drift", dict(d=2048 * 4000 + 1000)),
+    "n8_d16m_bf16_adam": ("n8_d16m_bf16_adam", dict(d=2048 * 9000 + 77)),
+    "n16_d256m_f32_ge_momentum": ("n16_d256m_f32_ge_momentum", dict(d=4096 * 3000 + 2056)),
+    "n200_bf16_adam": ("n64_llama7b_shard_bf16_adam", dict(n=200, d=4096 * 1500 + 1000)),
+    "n130_f32_sgd_drift": ("n64_d48m_f32_sgd_drift", dict(n=130, d=2048 * 1200 + 500)),
 }
 
 SCHEDULES = [
@@ -73,7 +76,8 @@ SCHEDULES = [
                                                        (False, False, False)])
 def test_paced_step_is_bit_identical_to_unpaced(name, sched, masks_out, drift, workspace,
                                                 restore_pacing):
-    w = wl.scaled(wl.WORKLOADS[name], **PACED[name])
+    base, sizes = PACED[name]
+    w = wl.scaled(wl.WORKLOADS[base], **sizes)
     if w.loss["kind"] == wl.GILBERT_ELLIOTT:
         workspace = True  # the chain scan needs it
     cfg = SCHEDULES[sched]
